@@ -1,0 +1,201 @@
+/*
+ * dlmc.h -- lossless compression with a masked diffusion language model on
+ * AMD MI355X (gfx950).  C ABI of libdlmc.so.
+ *
+ * Method: "Diffuse to Compress: Leveraging Diffusion LMs for Lossless
+ * Compression" (Nardone, Ferragina).  A sequence is split into independent
+ * non-overlapping windows ("chunks", Implementation Details).  Each chunk
+ * starts fully masked and is reconstructed over several inference steps
+ * (Diffusion-Based Compression Pipeline): one forward pass of a masked
+ * diffusion LM (Definition 3) gives a distribution at every masked position,
+ * the entropy-based commitment schedule (Symbol Commitment Schedules, item 3)
+ * picks positions, their symbols are coded with their predicted distributions
+ * by a statistical coder, and the symbols are revealed.  The schedule is
+ * deterministic, so the decoder replays it from the header alone (the remark
+ * closing Symbol Commitment Schedules).
+ *
+ * Conventions for every call:
+ *   - the return value is a dlmc_status: 0 on success, a negative code on
+ *     error; no C++ exception crosses the ABI; dlmc_last_error() gives a
+ *     thread-local message for the last failure on the calling thread;
+ *   - "host" pointers are caller-owned CPU memory, read or written during the
+ *     call only and never retained;
+ *   - "device" pointers are caller-owned GPU memory on the model's device
+ *     (e.g. torch tensors); the library reads / writes them on the model's
+ *     stream and never frees them;
+ *   - a dlmc_model handle is not thread safe: use one handle per host thread.
+ */
+#ifndef DLMC_H
+#define DLMC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t dlmc_status;
+#define DLMC_OK 0
+#define DLMC_E_INVAL -1   /* bad argument or unsupported configuration */
+#define DLMC_E_NOMEM -2   /* device or host allocation failed */
+#define DLMC_E_DEVICE -3  /* HIP runtime error */
+#define DLMC_E_FORMAT -4  /* not a dlmc container, or made by another model */
+#define DLMC_E_CORRUPT -5 /* bitstream fails to decode, or CRC mismatch */
+#define DLMC_E_BUFFER -6  /* output buffer too small; required size reported */
+#define DLMC_E_NUMERIC -7 /* non-finite logits or entropies */
+
+#define DLMC_FFN_GELU 0   /* x W1^T -> exact-erf GELU -> W2^T          */
+#define DLMC_FFN_SWIGLU 1 /* (silu(x Wg^T) * x Wu^T) Wd^T               */
+#define DLMC_NORM_LAYER 0 /* LayerNorm, gain 1, bias 0                  */
+#define DLMC_NORM_RMS 1   /* RMSNorm, gain 1                            */
+#define DLMC_DTYPE_F32 0  /* fp32 weights, activations and accumulation */
+#define DLMC_DTYPE_BF16 1 /* bf16 weights and GEMM inputs, fp32 accumulate,
+                             fp32 residual stream, norms, softmax, logits */
+
+/* Shape of the masked diffusion LM (Definition 3).  vocab = |Sigma|; the
+ * input-only [MASK] token id is vocab.  Weights are random: tensor entries
+ * are uniform on [-2^-e, 2^-e) from a counter-based generator (see
+ * dlmc_model_create) with e = the matching *_exp field. */
+typedef struct dlmc_model_config {
+  uint32_t struct_size; /* sizeof(dlmc_model_config) */
+  int32_t n_layers;     /* >= 0 */
+  int32_t d_model;      /* multiple of 64 (bf16) or 16 (f32) */
+  int32_t n_heads;      /* d_model / n_heads in {64, 128} (bf16), <= 128 (f32) */
+  int32_t d_ffn;        /* multiple of 64 (bf16) or 16 (f32) */
+  int32_t vocab;        /* |Sigma| >= 2; 2^cdf_bits must exceed it */
+  int32_t ffn_kind;     /* DLMC_FFN_* */
+  int32_t norm_kind;    /* DLMC_NORM_* */
+  int32_t dtype;        /* DLMC_DTYPE_* */
+  float rope_theta;     /* rotary base (rotate-half pairing of i, i + d_head/2) */
+  float norm_eps;
+  int32_t embed_exp, attn_exp, ffn_in_exp, ffn_out_exp, head_exp;
+  int32_t max_chunk; /* largest chunk length any call will use */
+  int32_t max_batch; /* largest number of chunks per forward pass */
+} dlmc_model_config;
+
+/* Commitment schedule and coder parameters (stored in the container header).
+ * Entropy-based schedule: commit every masked position whose entropy (bits)
+ * is <= tau_bits; if fewer than m_min qualify commit the m_min lowest; never
+ * more than m_max; ties by lower position; all remaining positions if fewer
+ * than m_min are masked.  tau_bits = -INFINITY with m_min = m_max = k is the
+ * fixed-k rule.  Committed symbols are coded in ascending position order. */
+typedef struct dlmc_codec_params {
+  uint32_t struct_size; /* sizeof(dlmc_codec_params) */
+  int32_t chunk_len;    /* window length w, 1..max_chunk */
+  float tau_bits;
+  int32_t m_min; /* >= 1 */
+  int32_t m_max; /* m_min..1024 */
+  int32_t cdf_bits;   /* P: CDF precision, 2^P > vocab, P <= coder_bits - 16 */
+  int32_t coder_bits; /* W: range coder width, 32 or 64 */
+  int32_t batch;      /* chunks per forward, 1..max_batch; does not change the output */
+  int32_t flags;      /* DLMC_FLAG_* */
+} dlmc_codec_params;
+
+#define DLMC_FLAG_CRC 1 /* store and check a CRC-32 of every chunk's tokens */
+
+typedef struct dlmc_model dlmc_model;
+typedef struct dlmc_session dlmc_session;
+
+/* ---- model ------------------------------------------------------------ */
+
+/* Create a model on HIP device `device` and generate its weights from
+ * `seed`: tensor t (embedding 1, head 2, layer l kind k -> 16 + 16 l + k with
+ * q,k,v,o,ffn_in,ffn_up,ffn_out = 0..6; all [out, in] row-major, embedding
+ * [vocab+1, d]) has entries w_i = ((u_i >> 40) - 2^23) 2^(-23-e) with
+ * u_i = splitmix64(splitmix64(seed ^ t*0x9E3779B97F4A7C15) + i), rounded to
+ * nearest-even bf16 for bf16 models.  The library owns the weights and the
+ * workspace for max_batch chunks of max_chunk tokens.
+ * Errors: E_INVAL (config), E_NOMEM, E_DEVICE. */
+dlmc_status dlmc_model_create(const dlmc_model_config* cfg, uint64_t seed, int32_t device,
+                              dlmc_model** out);
+/* Free the model and all its device memory.  NULL is ignored. */
+void dlmc_model_destroy(dlmc_model* model);
+/* Use `hip_stream` (a hipStream_t, e.g. torch.cuda.current_stream().cuda_stream)
+ * for all device work of this model; NULL selects the library's own stream. */
+dlmc_status dlmc_set_stream(dlmc_model* model, void* hip_stream);
+
+/* ---- compression ------------------------------------------------------- */
+
+/* Worst-case container size in bytes for n_tokens tokens. */
+dlmc_status dlmc_encode_bound(const dlmc_model* model, const dlmc_codec_params* codec,
+                              uint64_t n_tokens, uint64_t* bytes);
+/* Compress host tokens[0..n) (each in [0, vocab)) into the host buffer
+ * out[0..cap).  On E_BUFFER *out_len holds the required size. */
+dlmc_status dlmc_encode(dlmc_model* model, const dlmc_codec_params* codec,
+                        const int32_t* tokens, uint64_t n, uint8_t* out, uint64_t cap,
+                        uint64_t* out_len);
+/* Number of tokens a container holds (reads the header only; E_FORMAT). */
+dlmc_status dlmc_decode_size(const uint8_t* in, uint64_t len, uint64_t* n_tokens);
+/* Decompress host container in[0..len) into host tokens[0..cap).  The codec
+ * parameters come from the header; the batch used is `batch` when > 0, else
+ * the header's.  E_FORMAT if the container was made by a model with another
+ * configuration or seed; E_CORRUPT on an undecodable stream or CRC mismatch;
+ * E_BUFFER if cap is too small (*n = required). */
+dlmc_status dlmc_decode(dlmc_model* model, const uint8_t* in, uint64_t len, int32_t batch,
+                        int32_t* tokens, uint64_t cap, uint64_t* n);
+
+/* Streaming form of dlmc_encode: one call of dlmc_encoder_step runs exactly
+ * one masked-diffusion pass over the current batch of chunks (forward,
+ * entropy, selection, CDFs, coding, reveal).  `tokens` is copied at begin. */
+dlmc_status dlmc_encoder_begin(dlmc_model* model, const dlmc_codec_params* codec,
+                               const int32_t* tokens, uint64_t n, dlmc_session** out);
+/* *done = 1 once every chunk is coded; *coded (optional) += symbols coded. */
+dlmc_status dlmc_encoder_step(dlmc_session* s, int32_t* done, uint64_t* coded);
+/* Finish (running any remaining passes) and write the container. */
+dlmc_status dlmc_encoder_finish(dlmc_session* s, uint8_t* out, uint64_t cap, uint64_t* out_len);
+void dlmc_session_destroy(dlmc_session* s);
+
+/* Per (chunk, pass) trace of encode and decode: the committed positions
+ * (ascending), their entropies in bits, and an FNV-1a 64 hash of the
+ * committed rows' integer CDFs.  dir = 0 encode, 1 decode.  NULL disables. */
+typedef void (*dlmc_trace_fn)(void* user, int32_t dir, uint64_t chunk, int32_t pass,
+                              int32_t n_sel, const int32_t* pos, const float* entropy_bits,
+                              uint64_t cdf_hash);
+dlmc_status dlmc_set_trace(dlmc_model* model, dlmc_trace_fn fn, void* user);
+
+/* ---- stage hooks (device pointers; tests and benchmarks) ---------------- */
+
+/* One forward pass (Definition 3) over device state[B*T] (int32, MASK =
+ * vocab).  Writes the fp32 logits at the masked positions, in ascending
+ * (chunk, position) order, to logits[n_rows * vocab], their flat indices
+ * b*T + t to rows[n_rows], and n_rows to n_rows[0] (all device).  logits
+ * must hold B*T*vocab floats, rows B*T ints. */
+dlmc_status dlmc_forward_logits(dlmc_model* model, const int32_t* state, int32_t B, int32_t T,
+                                float* logits, int32_t* rows, int32_t* n_rows);
+/* Entropy (bits) and max of every row of device logits[n_rows * vocab], and
+ * the integer CDF of every row at precision cdf_bits: g[n_rows*vocab] =
+ * floor(exp(l - max) 2^24) and cdf[n_rows*(vocab+1)]; g and cdf may be NULL. */
+dlmc_status dlmc_entropy_cdf(dlmc_model* model, const float* logits, int32_t n_rows,
+                             int32_t cdf_bits, float* entropy_bits, float* row_max,
+                             uint32_t* g, uint32_t* cdf);
+/* The commitment schedule on device entropies: rows[n_rows] are flat b*T+t
+ * indices ascending (as from dlmc_forward_logits) with entropies H[n_rows].
+ * Writes per chunk b the committed positions sel_pos[b*m_max + j], their
+ * indices into rows sel_row[b*m_max + j] and the count n_sel[b]. */
+dlmc_status dlmc_select(dlmc_model* model, const float* entropy_bits, const int32_t* rows,
+                        int32_t n_rows, int32_t B, int32_t T, float tau_bits, int32_t m_min,
+                        int32_t m_max, int32_t* sel_pos, int32_t* sel_row, int32_t* n_sel);
+/* Copy weight tensor `tensor_id` (ids as in dlmc_model_create) to host dst in
+ * its canonical [out, in] layout: bf16 bit patterns (uint16) or fp32. */
+dlmc_status dlmc_weight_copy(dlmc_model* model, int32_t tensor_id, void* dst, uint64_t bytes);
+
+/* ---- host range coder hooks (no GPU needed) ----------------------------- */
+
+/* Range-code n symbol intervals [start_i, start_i + freq_i) of a 2^P total
+ * with the W-bit coder used inside the container; writes the flushed stream. */
+dlmc_status dlmc_rc_encode(const uint32_t* start, const uint32_t* freq, uint64_t n,
+                           int32_t cdf_bits, int32_t coder_bits, uint8_t* out, uint64_t cap,
+                           uint64_t* out_len);
+/* Decode n symbols, symbol i with host cdf[i*(V+1) .. i*(V+1)+V]. */
+dlmc_status dlmc_rc_decode(const uint8_t* in, uint64_t len, const uint32_t* cdf, uint64_t n,
+                           int32_t V, int32_t cdf_bits, int32_t coder_bits, int32_t* sym);
+
+/* ---- errors -------------------------------------------------------------- */
+const char* dlmc_status_string(dlmc_status s);
+const char* dlmc_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DLMC_H */

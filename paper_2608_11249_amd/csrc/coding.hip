@@ -1,0 +1,387 @@
+// Coding stages of one masked-diffusion step: masked-row compaction,
+// per-position entropy, the entropy-based commitment schedule, integer CDF
+// quantisation and the reveal of committed symbols.
+//
+// All reductions use fixed trees (wave butterflies, then wave totals in order)
+// and the CDF is integer arithmetic after one expf per entry, so encode and
+// decode compute bit-identical selections and CDFs.
+#include <climits>
+
+#include "kernels.h"
+
+namespace dlmc {
+namespace {
+
+// ---------------------------------------------------------------- compaction
+__global__ void __launch_bounds__(1024)
+compact_kernel(const int32_t* __restrict__ state, int B, int T, int mask_id,
+               int32_t* __restrict__ rows, int32_t* __restrict__ n_rows,
+               int32_t* __restrict__ chunk_off, int32_t* __restrict__ chunk_cnt) {
+  __shared__ int wcount[16];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int total = B * T;
+  int carry = 0;
+  for (int base = 0; base < total; base += 1024) {
+    const int i = base + tid;
+    const bool flag = i < total && state[i] == mask_id;
+    const uint64_t bal = __ballot(flag);
+    const int before = __popcll(bal & ((1ull << lane) - 1ull));
+    if (lane == 0) wcount[wave] = __popcll(bal);
+    __syncthreads();
+    int woff = 0, tile = 0;
+    for (int w = 0; w < 16; ++w) {
+      woff += w < wave ? wcount[w] : 0;
+      tile += wcount[w];
+    }
+    if (flag) rows[carry + woff + before] = i;
+    carry += tile;
+    __syncthreads();
+  }
+  if (tid == 0) n_rows[0] = carry;
+  __syncthreads();
+  // segment of chunk b: rows are ascending, find [b*T, (b+1)*T)
+  for (int b = tid; b < B; b += 1024) {
+    int lo = 0, hi = carry;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (rows[mid] < b * T) lo = mid + 1; else hi = mid;
+    }
+    int lo2 = lo, hi2 = carry;
+    while (lo2 < hi2) {
+      const int mid = (lo2 + hi2) >> 1;
+      if (rows[mid] < (b + 1) * T) lo2 = mid + 1; else hi2 = mid;
+    }
+    chunk_off[b] = lo;
+    chunk_cnt[b] = lo2 - lo;
+  }
+}
+
+// ---------------------------------------------------------------- entropy
+// Online softmax statistics of a set of logits relative to its max m:
+// Z = sum e^(l-m), A = sum e^(l-m) (l-m).  H_nats = ln Z - A / Z.
+struct Stat {
+  float m, Z, A;
+};
+
+__device__ __forceinline__ Stat merge(Stat x, Stat y) {
+  if (y.Z == 0.0f) return x;
+  if (x.Z == 0.0f) return y;
+  const float m = fmaxf(x.m, y.m);
+  const float cx = expf(x.m - m), cy = expf(y.m - m);
+  Stat r;
+  r.m = m;
+  r.Z = cx * x.Z + cy * y.Z;
+  r.A = cx * (x.A + (x.m - m) * x.Z) + cy * (y.A + (y.m - m) * y.Z);
+  return r;
+}
+
+__device__ __forceinline__ void add4(Stat& s, f32x4 v) {
+  const float mx = fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w));
+  if (mx > s.m) {
+    if (s.Z > 0.0f) {
+      const float c = expf(s.m - mx);
+      s.A = c * (s.A + (s.m - mx) * s.Z);
+      s.Z = c * s.Z;
+    }
+    s.m = mx;
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    if (v[e] == -INFINITY) continue;  // padding of a ragged row
+    const float t = v[e] - s.m;
+    const float p = expf(t);
+    s.Z += p;
+    s.A += p * t;
+  }
+}
+
+__global__ void __launch_bounds__(256)
+entropy_kernel(const float* __restrict__ logits, const int32_t* __restrict__ n_dev, int V,
+               float* __restrict__ H, float* __restrict__ mx) {
+  __shared__ Stat red[4];
+  const int row = blockIdx.x;
+  if (n_dev && row >= *n_dev) return;
+  const float* lg = logits + (size_t)row * V;
+  Stat s{-INFINITY, 0.0f, 0.0f};
+  if ((V & 3) == 0) {
+    for (int v = threadIdx.x * 4; v < V; v += 1024) add4(s, *reinterpret_cast<const f32x4*>(lg + v));
+  } else {
+    for (int v = threadIdx.x * 4; v < V; v += 1024) {
+      f32x4 x;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x[e] = v + e < V ? lg[v + e] : -INFINITY;
+      add4(s, x);
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    Stat t{__shfl_xor(s.m, o), __shfl_xor(s.Z, o), __shfl_xor(s.A, o)};
+    s = merge(s, t);
+  }
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    Stat r = merge(merge(merge(red[0], red[1]), red[2]), red[3]);
+    H[row] = (logf(r.Z) - r.A / r.Z) * 1.4426950408889634f;
+    mx[row] = r.m;
+  }
+}
+
+// ---------------------------------------------------------------- selection
+__device__ __forceinline__ uint32_t order_bits(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+template <typename K>
+__device__ void bitonic_sort(K* keys, int n2) {
+  for (int k = 2; k <= n2; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int i = threadIdx.x; i < n2; i += blockDim.x) {
+        const int ixj = i ^ j;
+        if (ixj > i) {
+          const K a = keys[i], b = keys[ixj];
+          const bool up = (i & k) == 0;
+          if ((a > b) == up) {
+            keys[i] = b;
+            keys[ixj] = a;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+constexpr int SEL_MAX_T = 8192;
+constexpr int SEL_MAX_M = 1024;
+
+// One workgroup per chunk: sort the chunk's masked positions by
+// (entropy, position), commit n = min(|M|, max(m_min, min(m_max, #{H <= tau})))
+// of them, and emit the committed positions in ascending order.
+__global__ void __launch_bounds__(1024)
+select_kernel(const float* __restrict__ H, const int32_t* __restrict__ rows,
+              const int32_t* __restrict__ chunk_off, const int32_t* __restrict__ chunk_cnt, int T,
+              float tau, int m_min, int m_max, int32_t* __restrict__ sel_pos,
+              int32_t* __restrict__ sel_row, int32_t* __restrict__ n_sel, int32_t* __restrict__ err) {
+  __shared__ uint64_t keys[SEL_MAX_T];
+  __shared__ int32_t chosen[SEL_MAX_M];
+  __shared__ int wsum[16], wbad[16];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int off = chunk_off[b], cnt = chunk_cnt[b];
+  int n2 = 1;
+  while (n2 < cnt) n2 <<= 1;
+  int thr = 0, bad = 0;
+  for (int i = tid; i < n2; i += 1024) {
+    uint64_t key = ~0ull;
+    if (i < cnt) {
+      const float h = H[off + i];
+      bad |= !(h == h) || isinf(h);
+      thr += h <= tau;
+      key = ((uint64_t)order_bits(h) << 32) | (uint32_t)i;
+    }
+    keys[i] = key;
+  }
+  // counts (integer: order-free)
+  int c = thr;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o);
+  const int anybad = __any(bad);
+  if ((tid & 63) == 0) {
+    wsum[tid >> 6] = c;
+    wbad[tid >> 6] = anybad;
+  }
+  __syncthreads();
+  int n_thr = 0, nbad = 0;
+  for (int w = 0; w < 16; ++w) {
+    n_thr += wsum[w];
+    nbad += wbad[w];
+  }
+  if (tid == 0 && nbad) err[0] = 1;
+  const int n = min(cnt, max(m_min, min(m_max, n_thr)));
+  bitonic_sort(keys, n2);
+  int n2s = 1;
+  while (n2s < n) n2s <<= 1;
+  for (int i = tid; i < n2s; i += 1024) chosen[i] = i < n ? (int32_t)(keys[i] & 0xFFFFFFFFu) : INT_MAX;
+  __syncthreads();
+  bitonic_sort(chosen, n2s);
+  for (int j = tid; j < n; j += 1024) {
+    const int local = chosen[j];
+    sel_pos[b * m_max + j] = rows[off + local] - b * T;
+    sel_row[b * m_max + j] = off + local;
+  }
+  if (tid == 0) n_sel[b] = n;
+}
+
+// ---------------------------------------------------------------- CDF
+__device__ __forceinline__ uint32_t gval(float l, float m) {
+  return (uint32_t)(expf(l - m) * 16777216.0f);  // floor(e * 2^24), e in [0, 1]
+}
+
+template <typename U>
+__device__ __forceinline__ U block_sum_int(U v, U* red) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return red[0] + red[1] + red[2] + red[3];
+}
+
+// integer CDF of one committed row:
+//   g_v = floor(exp(l_v - max) 2^24), G = sum g, f_v = 1 + floor(g_v (2^P - V) / G),
+//   the remainder 2^P - sum f goes to the lowest index of maximal g,
+//   cdf[0] = 0, cdf[v+1] = cdf[v] + f_v.
+__global__ void __launch_bounds__(256)
+cdf_kernel(const float* __restrict__ logits, const float* __restrict__ mx,
+           const int32_t* __restrict__ sel_row, const int32_t* __restrict__ n_sel, int m_max,
+           int V, int P, uint32_t* __restrict__ cdf, uint32_t* __restrict__ g_out) {
+  __shared__ uint64_t red64[4];
+  __shared__ int redi[4];
+  __shared__ uint32_t scan[4];
+  const int j = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (j >= n_sel[b]) return;
+  const int slot = b * m_max + j;
+  const int row = sel_row[slot];
+  const float* lg = logits + (size_t)row * V;
+  const float m = mx[row];
+  uint32_t* out = cdf + (size_t)slot * (V + 1);
+
+  uint64_t G = 0;
+  int a = INT_MAX;
+  for (int v = tid; v < V; v += 256) {
+    const uint32_t g = gval(lg[v], m);
+    G += g;
+    if (g == (1u << 24)) a = min(a, v);
+    if (g_out) g_out[(size_t)slot * V + v] = g;
+  }
+  G = block_sum_int<uint64_t>(G, red64);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) a = min(a, __shfl_xor(a, o));
+  if (lane == 0) redi[wave] = a;
+  __syncthreads();
+  a = min(min(redi[0], redi[1]), min(redi[2], redi[3]));
+
+  const uint64_t c = (1ull << P) - (uint64_t)V;
+  uint64_t F = 0;
+  for (int v = tid; v < V; v += 256) F += 1 + (uint64_t)gval(lg[v], m) * c / G;
+  F = block_sum_int<uint64_t>(F, red64);
+  const uint32_t R = (uint32_t)((1ull << P) - F);
+
+  if (tid == 0) out[0] = 0;
+  uint32_t carry = 0;
+  for (int base = 0; base < V; base += 1024) {
+    const int v0 = base + tid * 4;
+    uint32_t f[4], loc = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int v = v0 + e;
+      f[e] = v < V ? 1u + (uint32_t)((uint64_t)gval(lg[v], m) * c / G) + (v == a ? R : 0u) : 0u;
+      loc += f[e];
+    }
+    // exclusive scan of loc over the block (integer: order-free)
+    uint32_t inc = loc;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t t = __shfl_up(inc, o);
+      if (lane >= o) inc += t;
+    }
+    __syncthreads();
+    if (lane == 63) scan[wave] = inc;
+    __syncthreads();
+    uint32_t wpre = 0;
+    for (int w = 0; w < wave; ++w) wpre += scan[w];
+    uint32_t run = carry + wpre + inc - loc;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int v = v0 + e;
+      if (v < V) {
+        run += f[e];
+        out[v + 1] = run;
+      }
+    }
+    carry += scan[0] + scan[1] + scan[2] + scan[3];
+  }
+}
+
+// ---------------------------------------------------------------- reveal
+__global__ void gather_reveal_kernel(const uint32_t* __restrict__ cdf, const int32_t* __restrict__ sel_pos,
+                                     const int32_t* __restrict__ n_sel, const int32_t* __restrict__ tokens,
+                                     const int64_t* __restrict__ slot_base, int32_t* __restrict__ state,
+                                     int T, int m_max, int V, uint32_t* __restrict__ sym) {
+  const int b = blockIdx.x;
+  for (int j = threadIdx.x; j < n_sel[b]; j += blockDim.x) {
+    const int slot = b * m_max + j, pos = sel_pos[slot];
+    const int s = tokens[slot_base[b] + pos];
+    const uint32_t* c = cdf + (size_t)slot * (V + 1);
+    sym[2 * slot] = c[s];
+    sym[2 * slot + 1] = c[s + 1] - c[s];
+    state[(size_t)b * T + pos] = s;
+  }
+}
+
+__global__ void reveal_kernel(const int32_t* __restrict__ sel_pos, const int32_t* __restrict__ n_sel,
+                              const int32_t* __restrict__ dec, int32_t* __restrict__ state, int T,
+                              int m_max) {
+  const int b = blockIdx.x;
+  for (int j = threadIdx.x; j < n_sel[b]; j += blockDim.x) {
+    const int slot = b * m_max + j;
+    state[(size_t)b * T + sel_pos[slot]] = dec[slot];
+  }
+}
+
+}  // namespace
+
+void compact_masked(hipStream_t st, const int32_t* state, int B, int T, int mask_id,
+                    int32_t* rows, int32_t* n_rows, int32_t* chunk_off, int32_t* chunk_cnt) {
+  compact_kernel<<<1, 1024, 0, st>>>(state, B, T, mask_id, rows, n_rows, chunk_off, chunk_cnt);
+  DLMC_HIP(hipGetLastError());
+}
+
+void entropy_rows(hipStream_t st, const float* logits, int n_max, const int32_t* n_dev, int V,
+                  float* H, float* mx) {
+  if (n_max <= 0) return;
+  entropy_kernel<<<n_max, 256, 0, st>>>(logits, n_dev, V, H, mx);
+  DLMC_HIP(hipGetLastError());
+}
+
+void select_positions(hipStream_t st, const float* H, const int32_t* rows,
+                      const int32_t* chunk_off, const int32_t* chunk_cnt, int B, int T,
+                      float tau, int m_min, int m_max, int32_t* sel_pos, int32_t* sel_row,
+                      int32_t* n_sel, int32_t* err_flag) {
+  DLMC_CHECK(T <= SEL_MAX_T, DLMC_E_INVAL, "chunk length above 8192 is not supported");
+  DLMC_CHECK(m_min >= 1 && m_max >= m_min && m_max <= SEL_MAX_M, DLMC_E_INVAL,
+             "need 1 <= m_min <= m_max <= 1024");
+  if (B <= 0) return;
+  select_kernel<<<B, 1024, 0, st>>>(H, rows, chunk_off, chunk_cnt, T, tau, m_min, m_max, sel_pos,
+                                    sel_row, n_sel, err_flag);
+  DLMC_HIP(hipGetLastError());
+}
+
+void cdf_rows(hipStream_t st, const float* logits, const float* mx, const int32_t* sel_row,
+              const int32_t* n_sel, int B, int m_max, int V, int P, uint32_t* cdf,
+              uint32_t* g_out) {
+  if (B <= 0) return;
+  DLMC_CHECK(P <= 31 && (1ll << P) > V, DLMC_E_INVAL, "CDF precision must exceed the alphabet");
+  dim3 grid(m_max, B);
+  cdf_kernel<<<grid, 256, 0, st>>>(logits, mx, sel_row, n_sel, m_max, V, P, cdf, g_out);
+  DLMC_HIP(hipGetLastError());
+}
+
+void gather_reveal(hipStream_t st, const uint32_t* cdf, const int32_t* sel_pos,
+                   const int32_t* n_sel, const int32_t* tokens, const int64_t* slot_base,
+                   int32_t* state, int B, int T, int m_max, int V, uint32_t* sym) {
+  if (B <= 0) return;
+  gather_reveal_kernel<<<B, 256, 0, st>>>(cdf, sel_pos, n_sel, tokens, slot_base, state, T,
+                                          m_max, V, sym);
+  DLMC_HIP(hipGetLastError());
+}
+
+void reveal(hipStream_t st, const int32_t* sel_pos, const int32_t* n_sel, const int32_t* dec,
+            int32_t* state, int B, int T, int m_max) {
+  if (B <= 0) return;
+  reveal_kernel<<<B, 256, 0, st>>>(sel_pos, n_sel, dec, state, T, m_max);
+  DLMC_HIP(hipGetLastError());
+}
+
+}  // namespace dlmc

@@ -1,0 +1,300 @@
+// The masked diffusion LM (Definition 3 of the paper) on one GPU: weight
+// generation, workspace, and the launch sequence of one forward pass.
+#include <cmath>
+#include <cstring>
+
+#include "runtime.h"
+
+using namespace dlmc;
+
+dlmc_model::~dlmc_model() {
+  if (device >= 0) (void)hipSetDevice(device);
+  if (stream) (void)hipStreamSynchronize(stream);
+  for (void* p : allocs) (void)hipFree(p);
+  if (own_stream) (void)hipStreamDestroy(own_stream);
+}
+
+void* dlmc_model::dalloc(size_t bytes, bool zero) {
+  if (bytes == 0) bytes = 16;
+  void* p = nullptr;
+  if (hipMalloc(&p, bytes) != hipSuccess || !p) {
+    (void)hipGetLastError();
+    throw Error(DLMC_E_NOMEM, "hipMalloc of " + std::to_string(bytes) + " bytes failed");
+  }
+  allocs.push_back(p);
+  if (zero) DLMC_HIP(hipMemsetAsync(p, 0, bytes, stream));
+  return p;
+}
+
+void dlmc_model::dfree(void* p) {
+  if (!p) return;
+  for (auto it = allocs.begin(); it != allocs.end(); ++it)
+    if (*it == p) {
+      DLMC_HIP(hipStreamSynchronize(stream));
+      (void)hipFree(p);
+      allocs.erase(it);
+      return;
+    }
+}
+
+void dlmc_model::ensure_sel(int m_max) {
+  if (m_max <= sel_cap) return;
+  dfree(sel_pos);
+  dfree(sel_row);
+  dfree(n_sel);
+  dfree(dec);
+  dfree(cdf);
+  dfree(sym);
+  dfree(slot_base);
+  const size_t slots = (size_t)cfg.max_batch * m_max;
+  sel_pos = (int32_t*)dalloc(slots * 4, true);
+  sel_row = (int32_t*)dalloc(slots * 4, true);
+  dec = (int32_t*)dalloc(slots * 4, true);
+  n_sel = (int32_t*)dalloc((size_t)cfg.max_batch * 4, true);
+  cdf = (uint32_t*)dalloc(slots * (size_t)(cfg.vocab + 1) * 4);
+  sym = (uint32_t*)dalloc(slots * 8, true);
+  slot_base = (int64_t*)dalloc((size_t)cfg.max_batch * 8, true);
+  sel_cap = m_max;
+}
+
+void dlmc_model::ensure_tokens(size_t n) {
+  if (n <= tokens_cap && tokens_dev) return;
+  dfree(tokens_dev);
+  tokens_dev = (int32_t*)dalloc(std::max<size_t>(n, 1) * 4);
+  tokens_cap = n;
+}
+
+namespace dlmc {
+
+uint64_t fnv1a64(const void* data, size_t n, uint64_t h) {
+  const uint8_t* p = (const uint8_t*)data;
+  for (size_t i = 0; i < n; ++i) {
+    h ^= p[i];
+    h *= 0x100000001B3ull;
+  }
+  return h;
+}
+
+uint32_t crc32(const void* data, size_t n) {
+  static uint32_t table[256];
+  static bool init = false;
+  if (!init) {
+    for (uint32_t i = 0; i < 256; ++i) {
+      uint32_t c = i;
+      for (int k = 0; k < 8; ++k) c = (c & 1) ? 0xEDB88320u ^ (c >> 1) : c >> 1;
+      table[i] = c;
+    }
+    init = true;
+  }
+  uint32_t c = 0xFFFFFFFFu;
+  const uint8_t* p = (const uint8_t*)data;
+  for (size_t i = 0; i < n; ++i) c = table[(c ^ p[i]) & 0xFF] ^ (c >> 8);
+  return c ^ 0xFFFFFFFFu;
+}
+
+static void validate(const dlmc_model_config& c) {
+  DLMC_CHECK(c.struct_size == sizeof(dlmc_model_config), DLMC_E_INVAL, "config struct_size mismatch");
+  DLMC_CHECK(c.n_layers >= 0 && c.d_model > 0 && c.n_heads > 0 && c.d_ffn > 0, DLMC_E_INVAL,
+             "non-positive model dimension");
+  DLMC_CHECK(c.vocab >= 2 && c.vocab < (1 << 30), DLMC_E_INVAL, "vocab out of range");
+  DLMC_CHECK(c.d_model % c.n_heads == 0, DLMC_E_INVAL, "d_model must be a multiple of n_heads");
+  DLMC_CHECK(c.ffn_kind == DLMC_FFN_GELU || c.ffn_kind == DLMC_FFN_SWIGLU, DLMC_E_INVAL, "ffn_kind");
+  DLMC_CHECK(c.norm_kind == DLMC_NORM_LAYER || c.norm_kind == DLMC_NORM_RMS, DLMC_E_INVAL, "norm_kind");
+  DLMC_CHECK(c.dtype == DLMC_DTYPE_F32 || c.dtype == DLMC_DTYPE_BF16, DLMC_E_INVAL, "dtype");
+  DLMC_CHECK(c.max_chunk >= 1 && c.max_chunk <= 8192, DLMC_E_INVAL, "max_chunk must be in 1..8192");
+  DLMC_CHECK(c.max_batch >= 1 && (int64_t)c.max_batch * c.max_chunk <= (1 << 20), DLMC_E_INVAL,
+             "max_batch * max_chunk must be in 1..2^20");
+  DLMC_CHECK(c.d_model <= 8192, DLMC_E_INVAL, "d_model above 8192");
+  const int dh = c.d_model / c.n_heads;
+  if (c.dtype == DLMC_DTYPE_BF16) {
+    DLMC_CHECK(c.d_model % 64 == 0 && c.d_ffn % 64 == 0, DLMC_E_INVAL,
+               "bf16 model needs d_model and d_ffn multiples of 64");
+    DLMC_CHECK(dh == 64 || dh == 128, DLMC_E_INVAL, "bf16 model needs head dim 64 or 128");
+  } else {
+    DLMC_CHECK(c.d_model % 16 == 0 && c.d_ffn % 16 == 0, DLMC_E_INVAL,
+               "fp32 model needs d_model and d_ffn multiples of 16");
+    DLMC_CHECK(dh == 16 || dh == 32 || dh == 64 || dh == 128, DLMC_E_INVAL,
+               "fp32 model needs head dim 16, 32, 64 or 128");
+  }
+  const int exps[5] = {c.embed_exp, c.attn_exp, c.ffn_in_exp, c.ffn_out_exp, c.head_exp};
+  for (int e : exps) DLMC_CHECK(e >= -8 && e <= 60, DLMC_E_INVAL, "weight scale exponent out of range");
+  DLMC_CHECK(std::isfinite(c.rope_theta) && c.rope_theta > 1.0f, DLMC_E_INVAL, "rope_theta");
+  DLMC_CHECK(std::isfinite(c.norm_eps) && c.norm_eps >= 0.0f, DLMC_E_INVAL, "norm_eps");
+}
+
+void create_model(dlmc_model* m, const dlmc_model_config& cfg, uint64_t seed, int device) {
+  validate(cfg);
+  int ndev = 0;
+  DLMC_HIP(hipGetDeviceCount(&ndev));
+  DLMC_CHECK(device >= 0 && device < ndev, DLMC_E_INVAL, "no such HIP device");
+  m->device = device;
+  DLMC_HIP(hipSetDevice(device));
+  DLMC_HIP(hipStreamCreateWithFlags(&m->own_stream, hipStreamNonBlocking));
+  m->stream = m->own_stream;
+  m->cfg = cfg;
+  m->seed = seed;
+  m->bf16 = cfg.dtype == DLMC_DTYPE_BF16;
+  m->esz = m->bf16 ? 2 : 4;
+  const int d = cfg.d_model, F = cfg.d_ffn, V = cfg.vocab, L = cfg.n_layers, H = cfg.n_heads;
+  m->dh = d / H;
+  const int dh = m->dh, dt = cfg.dtype;
+  const bool glu = cfg.ffn_kind == DLMC_FFN_SWIGLU;
+  const int nF = glu ? 2 * F : F;
+  hipStream_t st = m->stream;
+
+  // ---- weights
+  m->embed = m->dalloc((size_t)(V + 1) * d * m->esz);
+  init_weights(st, m->embed, dt, seed, 1, V + 1, d, cfg.embed_exp, MAP_IDENTITY, 0, dh);
+  m->head = m->dalloc((size_t)V * d * m->esz);
+  init_weights(st, m->head, dt, seed, 2, V, d, cfg.head_exp, MAP_IDENTITY, 0, dh);
+  const RowMap qk_map = m->bf16 ? MAP_QK_PAIRS : MAP_IDENTITY;
+  for (int l = 0; l < L; ++l) {
+    dlmc_model::Layer w{};
+    const int base = 16 + 16 * l;
+    w.wqkv = m->dalloc((size_t)3 * d * d * m->esz);
+    init_weights(st, w.wqkv, dt, seed, base + 0, d, d, cfg.attn_exp, qk_map, 0, dh);
+    init_weights(st, w.wqkv, dt, seed, base + 1, d, d, cfg.attn_exp, qk_map, d, dh);
+    init_weights(st, w.wqkv, dt, seed, base + 2, d, d, cfg.attn_exp, MAP_IDENTITY, 2 * d, dh);
+    w.wo = m->dalloc((size_t)d * d * m->esz);
+    init_weights(st, w.wo, dt, seed, base + 3, d, d, cfg.attn_exp, MAP_IDENTITY, 0, dh);
+    w.win = m->dalloc((size_t)nF * d * m->esz);
+    if (glu && m->bf16) {
+      init_weights(st, w.win, dt, seed, base + 4, F, d, cfg.ffn_in_exp, MAP_GLU_PAIRS, 0, dh);
+      init_weights(st, w.win, dt, seed, base + 5, F, d, cfg.ffn_in_exp, MAP_GLU_PAIRS, 32, dh);
+    } else {
+      init_weights(st, w.win, dt, seed, base + 4, F, d, cfg.ffn_in_exp, MAP_IDENTITY, 0, dh);
+      if (glu) init_weights(st, w.win, dt, seed, base + 5, F, d, cfg.ffn_in_exp, MAP_IDENTITY, F, dh);
+    }
+    w.wout = m->dalloc((size_t)d * F * m->esz);
+    init_weights(st, w.wout, dt, seed, base + 6, d, F, cfg.ffn_out_exp, MAP_IDENTITY, 0, dh);
+    m->layers.push_back(w);
+  }
+
+  // ---- rotary table: angle = t * theta^(-2i/dh), computed in fp64
+  const int half = dh / 2, T = cfg.max_chunk;
+  std::vector<float> cs((size_t)T * half), sn((size_t)T * half);
+  for (int t = 0; t < T; ++t)
+    for (int i = 0; i < half; ++i) {
+      const double ang = (double)t * std::pow((double)cfg.rope_theta, -2.0 * i / dh);
+      cs[(size_t)t * half + i] = (float)std::cos(ang);
+      sn[(size_t)t * half + i] = (float)std::sin(ang);
+    }
+  m->rope_cos = (float*)m->dalloc(cs.size() * 4);
+  m->rope_sin = (float*)m->dalloc(sn.size() * 4);
+  DLMC_HIP(hipMemcpyAsync(m->rope_cos, cs.data(), cs.size() * 4, hipMemcpyHostToDevice, st));
+  DLMC_HIP(hipMemcpyAsync(m->rope_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice, st));
+
+  // ---- workspace
+  const size_t R = (size_t)cfg.max_batch * cfg.max_chunk;
+  m->max_rows = (int)R;
+  m->Tp_max = round_up(cfg.max_chunk, 128);
+  const size_t qkv_elems = (size_t)cfg.max_batch * H * m->Tp_max * dh;
+  m->x = (float*)m->dalloc(R * d * 4);
+  m->h = m->dalloc(R * d * m->esz);
+  // Q, K, V^T padding rows are read (with zero weight) by attention: keep them finite
+  m->q = m->dalloc(qkv_elems * m->esz, true);
+  m->k = m->dalloc(qkv_elems * m->esz, true);
+  m->vt = m->dalloc(qkv_elems * m->esz, true);
+  m->attn = m->dalloc(R * d * m->esz);
+  m->ffn = m->dalloc(R * F * m->esz);
+  if (!m->bf16) m->tmp = (float*)m->dalloc(R * std::max(3 * d, nF) * 4);
+  m->hm = m->dalloc(R * d * m->esz);
+  m->logits = (float*)m->dalloc(R * V * 4);
+  m->H = (float*)m->dalloc(R * 4);
+  m->mx = (float*)m->dalloc(R * 4);
+  m->rows = (int32_t*)m->dalloc(R * 4);
+  m->n_rows = (int32_t*)m->dalloc(4, true);
+  m->chunk_off = (int32_t*)m->dalloc((size_t)cfg.max_batch * 4);
+  m->chunk_cnt = (int32_t*)m->dalloc((size_t)cfg.max_batch * 4);
+  m->state = (int32_t*)m->dalloc(R * 4);
+  m->err = (int32_t*)m->dalloc(4, true);
+  DLMC_HIP(hipStreamSynchronize(st));
+}
+
+}  // namespace dlmc
+
+uint64_t dlmc_model::hash() const {
+  const int32_t f[] = {cfg.n_layers,  cfg.d_model,   cfg.n_heads,  cfg.d_ffn,
+                       cfg.vocab,     cfg.ffn_kind,  cfg.norm_kind, cfg.dtype,
+                       cfg.embed_exp, cfg.attn_exp,  cfg.ffn_in_exp, cfg.ffn_out_exp,
+                       cfg.head_exp};
+  uint64_t h = fnv1a64(f, sizeof(f));
+  uint32_t theta, eps;
+  std::memcpy(&theta, &cfg.rope_theta, 4);
+  std::memcpy(&eps, &cfg.norm_eps, 4);
+  h = fnv1a64(&theta, 4, h);
+  h = fnv1a64(&eps, 4, h);
+  return fnv1a64(&seed, 8, h);
+}
+
+void dlmc_model::forward(const int32_t* st_dev, int B, int T, float* logits_out, int32_t* rows_out,
+                         int32_t* n_rows_out) {
+  DLMC_CHECK(B >= 1 && B <= cfg.max_batch && T >= 1 && T <= cfg.max_chunk, DLMC_E_INVAL,
+             "batch / chunk length exceed the model's workspace");
+  const int d = cfg.d_model, F = cfg.d_ffn, V = cfg.vocab, H = cfg.n_heads;
+  const int M = B * T, Tp = round_up(T, 128);
+  const bool glu = cfg.ffn_kind == DLMC_FFN_SWIGLU;
+  const int nF = glu ? 2 * F : F;
+  float* lg = logits_out ? logits_out : logits;
+  int32_t* rw = rows_out ? rows_out : rows;
+  int32_t* nr = n_rows_out ? n_rows_out : n_rows;
+  hipStream_t s = stream;
+
+  dlmc::embed(s, st_dev, this->embed, cfg.dtype, x, M, d, V);
+  EpiArgs qkv;
+  qkv.q = q;
+  qkv.k = k;
+  qkv.vt = vt;
+  qkv.rope_cos = rope_cos;
+  qkv.rope_sin = rope_sin;
+  qkv.T = T;
+  qkv.Tp = Tp;
+  qkv.H = H;
+  qkv.dh = dh;
+  qkv.d = d;
+  EpiArgs resid;
+  resid.out = x;
+  resid.ldo = d;
+  for (const Layer& w : layers) {
+    norm_rows(s, x, h, cfg.dtype, M, d, cfg.norm_kind, cfg.norm_eps, nullptr, nullptr);
+    if (bf16) {
+      gemm_bf16(s, (const bf16_t*)h, (const bf16_t*)w.wqkv, M, 3 * d, d, nullptr, EPI_QKV_ROPE, qkv);
+      attention_bf16(s, (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)vt, (bf16_t*)attn, B, H, T, Tp, dh);
+      gemm_bf16(s, (const bf16_t*)attn, (const bf16_t*)w.wo, M, d, d, nullptr, EPI_RESIDUAL, resid);
+    } else {
+      EpiArgs t;
+      t.out = tmp;
+      t.ldo = 3 * d;
+      gemm_f32(s, (const float*)h, (const float*)w.wqkv, M, 3 * d, d, nullptr, EPI_STORE_F32, t);
+      qkv_rope_f32(s, tmp, M, qkv);
+      attention_f32(s, (const float*)q, (const float*)k, (const float*)vt, (float*)attn, B, H, T, Tp, dh);
+      gemm_f32(s, (const float*)attn, (const float*)w.wo, M, d, d, nullptr, EPI_RESIDUAL, resid);
+    }
+    norm_rows(s, x, h, cfg.dtype, M, d, cfg.norm_kind, cfg.norm_eps, nullptr, nullptr);
+    if (bf16) {
+      EpiArgs f;
+      f.out = ffn;
+      f.ldo = F;
+      gemm_bf16(s, (const bf16_t*)h, (const bf16_t*)w.win, M, nF, d, nullptr,
+                glu ? EPI_SWIGLU : EPI_GELU, f);
+      gemm_bf16(s, (const bf16_t*)ffn, (const bf16_t*)w.wout, M, d, F, nullptr, EPI_RESIDUAL, resid);
+    } else {
+      EpiArgs t;
+      t.out = tmp;
+      t.ldo = nF;
+      gemm_f32(s, (const float*)h, (const float*)w.win, M, nF, d, nullptr, EPI_STORE_F32, t);
+      ffn_act_f32(s, tmp, (float*)ffn, M, F, cfg.ffn_kind);
+      gemm_f32(s, (const float*)ffn, (const float*)w.wout, M, d, F, nullptr, EPI_RESIDUAL, resid);
+    }
+  }
+  // masked rows only: compaction, final norm gathered, LM head
+  compact_masked(s, st_dev, B, T, V, rw, nr, chunk_off, chunk_cnt);
+  norm_rows(s, x, hm, cfg.dtype, M, d, cfg.norm_kind, cfg.norm_eps, rw, nr);
+  EpiArgs o;
+  o.out = lg;
+  o.ldo = V;
+  if (bf16)
+    gemm_bf16(s, (const bf16_t*)hm, (const bf16_t*)this->head, M, V, d, nr, EPI_STORE_F32, o);
+  else
+    gemm_f32(s, (const float*)hm, (const float*)this->head, M, V, d, nr, EPI_STORE_F32, o);
+}

@@ -1,0 +1,113 @@
+// Internal runtime objects behind the C ABI: the model (weights + workspace)
+// and encode / decode sessions (the per-chunk pass loop).
+#pragma once
+
+#include <memory>
+#include <vector>
+
+#include "kernels.h"
+#include "range_coder.h"
+
+struct dlmc_model {
+  dlmc_model_config cfg{};
+  uint64_t seed = 0;
+  int device = 0;
+  hipStream_t stream = nullptr;      // stream in use
+  hipStream_t own_stream = nullptr;  // library-created stream
+  size_t esz = 2;                    // bytes per weight / GEMM-input element
+  bool bf16 = true;
+  int dh = 0;
+  std::vector<void*> allocs;
+
+  // weights (device): embedding [V+1, d]; per layer fused QKV [3d, d] (rotary
+  // pairs adjacent for bf16), O [d, d], FFN in [F or 2F, d] (gate/up pairs
+  // interleaved for bf16 SwiGLU), FFN out [d, F]; head [V, d]
+  void* embed = nullptr;
+  void* head = nullptr;
+  struct Layer {
+    void *wqkv, *wo, *win, *wout;
+  };
+  std::vector<Layer> layers;
+  float* rope_cos = nullptr;  // [max_chunk, dh/2]
+  float* rope_sin = nullptr;
+
+  // workspace for max_batch * max_chunk rows
+  int max_rows = 0, Tp_max = 0;
+  float* x = nullptr;  // fp32 residual stream [rows, d]
+  void *h = nullptr, *q = nullptr, *k = nullptr, *vt = nullptr, *attn = nullptr, *ffn = nullptr;
+  float* tmp = nullptr;  // fp32 model only: [rows, max(3d, 2F)]
+  void* hm = nullptr;    // final-norm rows of masked positions [rows, d]
+  float* logits = nullptr;  // [rows, V]
+  float *H = nullptr, *mx = nullptr;
+  int32_t *rows = nullptr, *n_rows = nullptr, *chunk_off = nullptr, *chunk_cnt = nullptr;
+  int32_t *state = nullptr, *err = nullptr;
+
+  // selection buffers, grown on demand: max_batch * sel_cap slots
+  int sel_cap = 0;
+  int32_t *sel_pos = nullptr, *sel_row = nullptr, *n_sel = nullptr, *dec = nullptr;
+  uint32_t *cdf = nullptr, *sym = nullptr;
+  int64_t* slot_base = nullptr;
+  int32_t* tokens_dev = nullptr;
+  size_t tokens_cap = 0;
+
+  dlmc_trace_fn trace = nullptr;
+  void* trace_user = nullptr;
+
+  ~dlmc_model();
+  void* dalloc(size_t bytes, bool zero = false);
+  void dfree(void* p);
+  void ensure_sel(int m_max);
+  void ensure_tokens(size_t n);
+  uint64_t hash() const;
+  // One forward pass over state[B*T] (device): logits at masked rows into
+  // logits_out (or the internal buffer), row ids and count likewise.
+  void forward(const int32_t* state, int B, int T, float* logits_out, int32_t* rows_out,
+               int32_t* n_rows_out);
+};
+
+namespace dlmc {
+
+uint64_t fnv1a64(const void* data, size_t n, uint64_t h = 0xCBF29CE484222325ull);
+uint32_t crc32(const void* data, size_t n);
+void create_model(dlmc_model* m, const dlmc_model_config& cfg, uint64_t seed, int device);
+void validate_codec(const dlmc_model* m, const dlmc_codec_params& cp);
+
+}  // namespace dlmc
+
+struct dlmc_session {
+  dlmc_model* m = nullptr;
+  dlmc_codec_params cp{};
+  bool encode = true;
+  uint64_t n = 0;
+  std::vector<int32_t> tokens;     // encode input / decode output
+  std::vector<std::vector<uint8_t>> payload;  // per chunk (encode output / decode input)
+  std::vector<uint32_t> crc;                  // per chunk (decode: expected)
+  uint64_t n_chunks = 0, n_full = 0;
+  int last_len = 0;
+
+  // pass-loop state
+  int phase = 0;  // 0: full-length chunks, 1: the final partial chunk, 2: done
+  int B = 0, T = 0;
+  uint64_t next_chunk = 0;
+  std::vector<int64_t> slot_chunk;
+  std::vector<int> slot_left, slot_pass;
+  std::vector<dlmc::RangeEncoder> encs;
+  std::vector<dlmc::RangeDecoder> decs;
+  bool started = false;
+  uint64_t passes = 0;
+
+  // pinned host staging
+  int32_t* h_nsel = nullptr;
+  int32_t* h_pos = nullptr;
+  int32_t* h_err = nullptr;
+  uint32_t* h_sym = nullptr;
+  uint32_t* h_cdf = nullptr;  // decode / trace: sel_cap * (V+1) per slot
+  int32_t* h_dec = nullptr;
+  int64_t* h_base = nullptr;
+
+  ~dlmc_session();
+  void begin_phase();
+  void assign(int b, uint64_t chunk);
+  int step(uint64_t* coded);  // returns 1 when done
+  std::vector<uint8_t> container() const;
+};

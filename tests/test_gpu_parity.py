@@ -1,0 +1,242 @@
+"""GPU parity of the HIP path against the CPU oracle, through the C ABI.
+
+Tolerances (logits, per row max |gpu - oracle| / max |oracle|): 1e-5 for the
+fp32 model, 2e-2 for bf16 models.  Integer work (selection, CDFs given the
+GPU's own g, round trips) is compared bit-exactly.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import workloads as wl
+from oracle import cdf as OC
+from oracle import driver as OD
+from oracle import model as OM
+from oracle import schedule as OS
+from oracle import weights as OW
+
+from gpu_common import codec, log, payloads, rel_err_rows, shape
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+import paper_2608_11249_amd as dl  # noqa: E402
+
+
+def dev_state(state):
+    return torch.from_numpy(np.ascontiguousarray(state, dtype=np.int32)).cuda()
+
+
+# ---------------------------------------------------------------- weights
+@pytest.mark.parametrize("sh", [
+    shape(dtype="f32", d_model=64, n_heads=2, d_ffn=96),
+    shape(dtype="bf16", ffn="swiglu", norm="rmsnorm"),
+    shape(dtype="bf16", d_model=256, n_heads=2, d_ffn=256, ffn="swiglu", norm="rmsnorm", n_layers=1),
+])
+def test_weights_bit_identical_to_oracle(sh):
+    log("weights", sh)
+    W = OW.Weights(sh)
+    with dl.Model(sh, max_chunk=8) as m:
+        d, F, V = sh.d_model, sh.d_ffn, sh.vocab
+        cases = [(1, V + 1, d, sh.embed_exp), (2, V, d, sh.head_exp)]
+        for l in range(sh.n_layers):
+            b = 16 + 16 * l
+            cases += [(b, d, d, sh.attn_exp), (b + 1, d, d, sh.attn_exp), (b + 2, d, d, sh.attn_exp),
+                      (b + 3, d, d, sh.attn_exp), (b + 4, F, d, sh.ffn_in_exp),
+                      (b + 6, d, F, sh.ffn_out_exp)]
+            if sh.ffn == "swiglu":
+                cases.append((b + 5, F, d, sh.ffn_in_exp))
+        for tid, rows, cols, e in cases:
+            got = m.weight(tid, rows, cols)
+            ref = OW.gen_tensor(sh.seed, tid, (rows, cols), e, sh.dtype)
+            if sh.dtype == "bf16":
+                assert np.array_equal(got, OW.bf16_bits(ref)), tid
+            else:
+                assert np.array_equal(got, ref.astype(np.float32)), tid
+
+
+# ---------------------------------------------------------------- forward
+def check_logits(sh, B, T, mask_frac, tol, seed=0):
+    log("logits", sh.name, sh.dtype, f"L={sh.n_layers} d={sh.d_model} B={B} T={T}")
+    W = OW.Weights(sh)
+    st = wl.random_state(seed, B, T, sh.vocab, mask_frac)
+    st[:, 0] = sh.mask_id
+    with dl.Model(sh, max_chunk=T, max_batch=B) as m:
+        lg, rows = m.forward_logits(dev_state(st))
+        lg, rows = lg.cpu().numpy(), rows.cpu().numpy()
+    ref_rows, errs = [], []
+    for b in range(B):
+        ref, pos = OM.logits(sh, W, st[b])
+        ref_rows.extend(b * T + pos)
+        sel = (rows >= b * T) & (rows < (b + 1) * T)
+        errs.append(rel_err_rows(lg[sel], ref))
+    assert np.array_equal(rows, np.array(ref_rows))
+    err = max(errs)
+    log("max rel err", err)
+    assert err <= tol, err
+    return lg, rows
+
+
+@pytest.mark.parametrize("B,T", [(3, 256), (2, 100), (1, 1), (1, 77)])
+def test_logits_fp32_tiny(B, T):
+    check_logits(wl.TINY, B, T, 0.5, 1e-5)
+
+
+@pytest.mark.parametrize("kw,B,T", [
+    (dict(), 2, 100),
+    (dict(ffn="swiglu", norm="rmsnorm"), 3, 130),
+    (dict(d_model=256, n_heads=2, ffn="swiglu", norm="rmsnorm", vocab=1000), 2, 257),
+    (dict(d_model=256, n_heads=4, d_ffn=512, vocab=333), 1, 64),
+])
+def test_logits_bf16_small_shapes(kw, B, T):
+    check_logits(shape(**kw), B, T, 0.6, 2e-2)
+
+
+def test_logits_bf16_small_config():
+    sh = wl.WORKLOADS["small"].model
+    check_logits(sh, 1, 1024, 0.7, 2e-2)
+
+
+def test_logits_batch_invariant():
+    sh = shape(ffn="swiglu", norm="rmsnorm")
+    st = wl.random_state(5, 4, 96, sh.vocab, 0.5)
+    with dl.Model(sh, max_chunk=96, max_batch=4) as m:
+        lg, rows = m.forward_logits(dev_state(st))
+        lg = lg.cpu().numpy()
+        rows = rows.cpu().numpy()
+        for b in (0, 3):
+            one, r1 = m.forward_logits(dev_state(st[b:b + 1]))
+            sel = (rows >= b * 96) & (rows < (b + 1) * 96)
+            assert np.array_equal(one.cpu().numpy(), lg[sel])
+
+
+# ---------------------------------------------------------------- entropy / CDF
+@pytest.mark.parametrize("V,P,scale", [(256, 16, 3.0), (1001, 16, 8.0), (32768, 24, 2.0),
+                                       (126464, 24, 9.0)])
+def test_entropy_and_cdf_kernels(V, P, scale):
+    log("entropy/cdf", V, P)
+    sh = shape(vocab=V, n_layers=0)
+    lg = wl.random_logits(V + 1, 24, V, scale)
+    lg[3] = 0.0                     # uniform row
+    lg[4] = -50.0
+    lg[4, 7] = 10.0                 # one dominant symbol
+    with dl.Model(sh, max_chunk=8) as m:
+        H, mx, g, cdf = m.entropy_cdf(torch.from_numpy(lg).cuda(), P)
+        H, mx, g, cdf = (t.cpu().numpy() for t in (H, mx, g, cdf))
+    g = g.view(np.uint32).astype(np.int64)
+    cdf = cdf.view(np.uint32).astype(np.int64)
+    Href = OS.entropy_bits(lg.astype(np.float64))
+    assert np.max(np.abs(H - Href)) <= 1e-3, np.max(np.abs(H - Href))
+    assert np.array_equal(mx, lg.max(axis=1))
+    for i in range(len(lg)):
+        gref = OC.quantise_g(lg[i])
+        assert np.max(np.abs(g[i] - gref)) <= 2
+        # the integer stage is bit-exact given the GPU's own g
+        assert np.array_equal(cdf[i], OC.integer_cdf(g[i], P)), i
+
+
+# ---------------------------------------------------------------- selection
+@pytest.mark.parametrize("tau,mmin,mmax", [(float("-inf"), 4, 4), (0.5, 1, 64), (3.0, 2, 5),
+                                           (100.0, 1, 16), (float("-inf"), 64, 64)])
+def test_select_kernel_exact(tau, mmin, mmax):
+    log("select", tau, mmin, mmax)
+    B, T = 5, 300
+    rng = np.random.default_rng(mmax)
+    st = wl.random_state(9, B, T, 10, 0.6)
+    st[3] = 0                       # a chunk with nothing masked
+    st[4] = 10                      # fully masked
+    rows = np.nonzero(st.reshape(-1) == 10)[0].astype(np.int32)
+    H = np.round(rng.uniform(0, 6, len(rows)), 1).astype(np.float32)   # many ties
+    sh = shape(vocab=10, n_layers=0)
+    with dl.Model(sh, max_chunk=T, max_batch=B) as m:
+        sp, sr, ns = m.select(torch.from_numpy(H).cuda(), torch.from_numpy(rows).cuda(), B, T,
+                              tau, mmin, mmax)
+        sp, sr, ns = sp.cpu().numpy(), sr.cpu().numpy(), ns.cpu().numpy()
+    for b in range(B):
+        seg = (rows >= b * T) & (rows < (b + 1) * T)
+        pos = rows[seg] - b * T
+        ref = OS.select(H[seg].astype(np.float64), pos, tau, mmin, mmax)
+        assert ns[b] == len(ref)
+        assert np.array_equal(sp[b, : ns[b]], ref)
+        assert np.array_equal(rows[sr[b, : ns[b]]] - b * T, ref)
+
+
+# ---------------------------------------------------------------- round trips
+def roundtrip(m, toks, cd, batch_dec=0, crc=False):
+    data = m.encode(toks, cd, crc=crc)
+    back = m.decode(data, batch=batch_dec)
+    assert np.array_equal(back, toks)
+    return data
+
+
+def test_roundtrip_tiny_workload_full_with_trace_and_code_length():
+    w = wl.WORKLOADS["tiny"]
+    toks = wl.make_tokens(w)
+    log("tiny round trip", len(toks))
+    traces = {0: {}, 1: {}}
+
+    def tr(d, chunk, pas, pos, ent, h):
+        traces[d][(chunk, pas)] = (tuple(pos), tuple(ent), h)
+
+    with dl.Model(w.model, max_chunk=w.codec.chunk_len, max_batch=w.codec.batch) as m:
+        m.set_trace(tr)
+        data = roundtrip(m, toks, w.codec)
+        m.set_trace(None)
+    # encode and decode made bit-identical decisions and CDFs
+    assert traces[0] == traces[1] and len(traces[0]) == 16 * 64
+    # code length against the oracle replaying the GPU's trajectory
+    W = OW.Weights(w.model)
+    gpu_bytes = [len(p) for p in payloads(data)]
+    for c in (0, 7):
+        forced = [np.array(traces[0][(c, p)][0]) for p in range(64)]
+        seg = toks[c * 256:(c + 1) * 256]
+        r = OD.encode_chunk(w.model, W, seg, w.codec, forced=forced)
+        assert abs(gpu_bytes[c] - len(r.payload)) / len(r.payload) <= 0.005 + 4.0 / len(r.payload)
+        assert abs(gpu_bytes[c] * 8 - 32 - r.coded_bits) / r.coded_bits <= 0.005 + 16 / r.coded_bits
+
+
+@pytest.mark.parametrize("dec_batch", [1, 3])
+def test_roundtrip_batch_invariance(dec_batch):
+    sh = shape(ffn="swiglu", norm="rmsnorm")
+    cd = codec(64, k=5, batch=4)
+    toks = wl.markov1_tokens(64 * 5 + 17, sh.vocab, 12)
+    log("batch invariance", dec_batch)
+    with dl.Model(sh, max_chunk=64, max_batch=4) as m:
+        a = roundtrip(m, toks, cd, batch_dec=dec_batch)
+        b = m.encode(toks, cd, batch=1)
+    assert payloads(a) == payloads(b)
+
+
+@pytest.mark.parametrize("kw,cd,n", [
+    (dict(), codec(100, tau=4.0, mmin=1, mmax=8, batch=3), 350),
+    (dict(ffn="swiglu", norm="rmsnorm", vocab=70000), codec(128, k=16, P=24, W=64, batch=2), 300),
+    (dict(dtype="f32", d_model=64, n_heads=4, d_ffn=64, vocab=256), codec(50, k=7, batch=2), 123),
+])
+def test_roundtrip_schedules_and_coders(kw, cd, n):
+    sh = shape(**kw)
+    toks = wl.markov1_tokens(n, sh.vocab, 4)
+    log("roundtrip", kw, cd)
+    with dl.Model(sh, max_chunk=cd.chunk_len, max_batch=cd.batch) as m:
+        roundtrip(m, toks, cd, crc=True)
+
+
+def test_errors_on_gpu_model():
+    sh = shape()
+    cd = codec(32, k=4)
+    toks = wl.markov1_tokens(70, sh.vocab, 1)
+    with dl.Model(sh, max_chunk=32) as m:
+        data = m.encode(toks, cd, crc=True)
+        bad = bytearray(data)
+        bad[-3] ^= 0x5A
+        with pytest.raises(dl.DlmcError) as e:
+            m.decode(bytes(bad))
+        assert e.value.code in (-5,)
+        with pytest.raises(dl.DlmcError) as e:
+            m.encode(np.array([0, 1, sh.vocab]), cd)
+        assert e.value.code == -1
+    other = shape(seed=4)
+    with dl.Model(other, max_chunk=32) as m2:
+        with pytest.raises(dl.DlmcError) as e:
+            m2.decode(data)
+        assert e.value.code == -4

@@ -1,0 +1,93 @@
+"""Host-side checks of libdlmc.so that need no GPU: every declared symbol is
+exported, and the host range coder inside the library is byte-identical to the
+oracle's coder."""
+import ctypes
+import math
+import os
+
+import numpy as np
+import pytest
+
+import paper_2608_11249_amd as dl
+from oracle import cdf as OC
+from oracle import coder as ORC
+
+pytestmark = pytest.mark.skipif(not os.path.exists(dl.LIB_PATH), reason="libdlmc.so not built")
+
+
+def test_library_exports_every_declared_symbol():
+    L = ctypes.CDLL(dl.LIB_PATH)
+    names = dl.header_symbols()
+    assert len(names) >= 20
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(dl._SIGS)
+
+
+def random_stream(rng, n, V, P):
+    cdfs, syms = [], []
+    for _ in range(n):
+        w = rng.dirichlet(np.full(V, 0.2))
+        c = OC.cdf_row(np.log(np.maximum(w, 1e-300)), P)
+        cdfs.append(c)
+        syms.append(int(rng.choice(V, p=np.diff(c) / 2.0 ** P)))
+    return np.array(cdfs, dtype=np.uint32), np.array(syms)
+
+
+@pytest.mark.parametrize("W,P,V,n", [(32, 16, 256, 700), (64, 24, 300, 500), (32, 16, 2, 64),
+                                     (64, 24, 5000, 40), (32, 16, 256, 0)])
+def test_host_coder_matches_oracle_bytes(W, P, V, n):
+    rng = np.random.default_rng(W * 7 + V)
+    cdfs, syms = random_stream(rng, n, V, P)
+    start = cdfs[np.arange(n), syms] if n else np.zeros(0, np.uint32)
+    freq = (cdfs[np.arange(n), syms + 1] - start) if n else np.zeros(0, np.uint32)
+    ours = dl.rc_encode(start, freq, P, W)
+    enc = ORC.RangeEncoder(W, P)
+    for s, f in zip(start, freq):
+        enc.encode(int(s), int(f))
+    assert ours == enc.finish()
+    if n:
+        assert np.array_equal(dl.rc_decode(ours, cdfs, P, W), syms)
+
+
+def test_host_coder_carry_heavy_stream():
+    # near-certain symbols at the top of the range force long 0xFF runs and carries
+    P, W = 16, 32
+    start = np.full(3000, (1 << P) - 2, dtype=np.uint32)
+    freq = np.ones(3000, dtype=np.uint32)
+    start[::7] = 0
+    freq[::7] = (1 << P) - 2
+    ours = dl.rc_encode(start, freq, P, W)
+    enc = ORC.RangeEncoder(W, P)
+    for s, f in zip(start, freq):
+        enc.encode(int(s), int(f))
+    assert ours == enc.finish()
+
+
+def test_host_coder_rejects_bad_input():
+    with pytest.raises(dl.DlmcError) as e:
+        dl.rc_encode([0], [0], 16, 32)
+    assert e.value.code == -1
+    with pytest.raises(dl.DlmcError) as e:
+        dl.rc_encode([1 << 16], [1], 16, 32)
+    assert e.value.code == -1
+    with pytest.raises(dl.DlmcError) as e:
+        dl.rc_encode([0], [1], 20, 32)          # P > W - 16
+    assert e.value.code == -1
+    cdf = np.array([[0, 1, 1 << 16]], dtype=np.uint32)
+    with pytest.raises(dl.DlmcError) as e:
+        dl.rc_decode(b"\xff" * 8, cdf, 16, 32)
+    assert e.value.code == -5
+
+
+def test_decode_size_rejects_garbage():
+    for bad in (b"", b"XXXX" + bytes(100), b"DLMC" + bytes(20)):
+        with pytest.raises(dl.DlmcError) as e:
+            dl.decode_size(bad)
+        assert e.value.code == -4
+
+
+def test_status_strings():
+    L = dl.lib()
+    for code in range(-7, 1):
+        assert L.dlmc_status_string(code)
