@@ -1,0 +1,194 @@
+#!/usr/bin/env python
+"""Throughput of DLM-based lossless compression on one MI355X.
+
+A step is one masked-diffusion encode pass over one batch of chunks: the
+bidirectional transformer forward over every position, entropy of every
+masked position, the commitment schedule, integer CDFs of the committed
+positions, range coding on the host and the reveal.  The default workload is
+the 8B-shaped model (32 layers, d=4096, 32 heads, SwiGLU 12288, vocab 126464)
+on 2048-token chunks with k=16 positions per pass; the input is a seeded
+synthetic order-1 Zipf/Markov token stream (u32 tokens) standing in for the
+paper's tokenised enwik8, and the weights are seeded random.
+
+value = input bytes encoded per second over the timed steps (tokens are
+resident in HBM before timing starts).  roofline = the dominant kernel's
+algorithmic flops per launch / its average HIP-event duration in the timed
+region, against the bf16 dense MFMA peak.  cpu_baseline = the fp64 CPU oracle
+on a bounded sample of one pass, extrapolated to the same unit.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3    # MI355X fp32 vector
+PEAK_HBM_GBS = 8000.0
+
+
+def needed_tokens(w, steps):
+    cd = w.codec
+    T, B = cd.chunk_len, cd.batch
+    min_passes = math.ceil(T / cd.m_max)          # a chunk lasts at least this many passes
+    chunks = B * (math.ceil(steps / min_passes) + 1)
+    return min(w.n_tokens, chunks * T)
+
+
+def cpu_baseline(w, layers_timed=1, vocab_sample=4096):
+    """Time the oracle on one pass of one chunk with half its positions masked:
+    `layers_timed` of the model's layers at full width (x n_layers), the LM head
+    against a `vocab_sample`-row slice of the head (x vocab / sample), entropy
+    of the masked rows, selection, and k full-vocabulary CDF rows."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    import workloads as wl
+    from oracle import cdf as OC
+    from oracle import model as OM
+    from oracle import schedule as OS
+    from oracle import weights as OW
+
+    sh, cd = w.model, w.codec
+    T, V, k = cd.chunk_len, sh.vocab, cd.m_max
+    W = OW.Weights(sh)
+    st = np.full(T, sh.mask_id)
+    st[::2] = wl.make_tokens(w, T)[::2]
+    x = W.embed_rows(st)
+    cos, sin = OM.rope_cos_sin(T, sh.d_head, sh.rope_theta)
+    lw = [W.layer(l) for l in range(layers_timed)]           # generation is not timed
+    vs = min(V, vocab_sample)
+    head = W.head_rows(np.arange(vs))
+    full_row = wl.random_logits(1, 1, V, 8.0)[0].astype(np.float64)
+
+    t0 = time.perf_counter()
+    for l in range(layers_timed):
+        x = OM.block(sh, lw[l], x, cos, sin)
+    t_layers = (time.perf_counter() - t0) / layers_timed
+    t0 = time.perf_counter()
+    pos = OM.masked_positions(sh, st)
+    h = OM.norm(sh, x)[pos]
+    lg = h @ head.T
+    H = OS.entropy_bits(lg)
+    t_head = (time.perf_counter() - t0) * V / vs
+    t0 = time.perf_counter()
+    OS.select(H, pos, cd.tau_bits, cd.m_min, cd.m_max)
+    for _ in range(k):
+        OC.cdf_row(full_row, cd.cdf_bits)
+    t_rest = time.perf_counter() - t0
+    t_pass = sh.n_layers * t_layers + t_head + t_rest
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    return {
+        "value": k * w.token_bytes / t_pass,
+        "unit": "B/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": (f"one pass of one {T}-token chunk, {T // 2} masked: {layers_timed} of "
+                   f"{sh.n_layers} layers timed (x{sh.n_layers}), LM head on a {vs}-row vocab "
+                   f"slice (x{V / vs:.1f}), entropy, selection, {k} CDF rows; "
+                   f"fp64 NumPy, extrapolated pass time {t_pass:.1f} s"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="8b",
+                    choices=["tiny", "small", "8b", "8b-throughput", "8b-long"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: the compression path shards by independent "
+              "chunks (see DESIGN.md); --gpus must be 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2608_11249_amd as dl
+    import workloads as wl
+
+    w = wl.WORKLOADS[args.workload]
+    sh, cd = w.model, w.codec
+    toks = wl.make_tokens(w, needed_tokens(w, args.warmup + args.steps))
+    torch.cuda.init()
+    model = dl.Model(sh, max_chunk=cd.chunk_len, max_batch=cd.batch)
+    enc = model.encoder(cd, toks)
+    for _ in range(args.warmup):
+        enc.step()
+    torch.cuda.synchronize()
+    model.profile(True)
+    c0 = enc.coded
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    steps = 0
+    for _ in range(args.steps):
+        done = enc.step()
+        steps += 1
+        if done:
+            break
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    prof = model.profile_read()
+    model.profile(False)
+    coded = enc.coded - c0
+
+    bf16 = sh.dtype == "bf16"
+    gemm_stages = ["qkv", "attn", "oproj", "ffn_in", "ffn_out", "head"]
+    dom = max(gemm_stages, key=lambda s: prof[s][0])
+    ms, n, work = prof[dom]
+    achieved = (work / n) / (ms / n * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if bf16 else PEAK_FP32_TFLOPS
+    step_flops = sum(prof[s][2] for s in gemm_stages) / steps
+    stages_ms = {s: round(v[0] / steps, 3) for s, v in prof.items() if v[1]}
+    out = {
+        "metric": "input bytes/s encoded per MI355X (8B-shaped DLM)",
+        "value": coded * w.token_bytes / elapsed,
+        "unit": "B/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": args.warmup,
+        "ms_per_step": elapsed / steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": sh.dtype,
+        "data": "synthetic (seeded order-1 Zipf/Markov token stream; seeded random weights)",
+        "config": {
+            "workload": f"{w.name}: L={sh.n_layers} d={sh.d_model} heads={sh.n_heads} "
+                        f"ffn={sh.d_ffn} {sh.ffn} vocab={sh.vocab}, chunk {cd.chunk_len} x "
+                        f"batch {cd.batch}, {'k=%d' % cd.m_max if cd.m_min == cd.m_max else 'H<=%.2g bits, %d..%d' % (cd.tau_bits, cd.m_min, cd.m_max)} per pass",
+            "token_bytes": w.token_bytes,
+            "cdf_bits": cd.cdf_bits,
+            "coder_bits": cd.coder_bits,
+        },
+        "roofline": {
+            "bound": "mfma" if bf16 else "alu",
+            "kernel": f"{dom} GEMM" if dom != "attn" else "attention",
+            "achieved": round(achieved, 1),
+            "peak": peak,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / peak, 4),
+            "traffic": None,
+        },
+        "detail": {
+            "tokens_per_s": coded / elapsed,
+            "forward_tokens_per_s": steps * cd.batch * cd.chunk_len / elapsed,
+            "step_tflops": round(step_flops / (elapsed / steps) / 1e12, 1),
+            "step_mfma_frac": round(step_flops / (elapsed / steps) / 1e12 / peak, 4),
+            "stage_ms_per_step": stages_ms,
+        },
+    }
+    model.close()
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -180,6 +180,31 @@ dlmc_status dlmc_select(dlmc_model* model, const float* entropy_bits, const int3
  * its canonical [out, in] layout: bf16 bit patterns (uint16) or fp32. */
 dlmc_status dlmc_weight_copy(dlmc_model* model, int32_t tensor_id, void* dst, uint64_t bytes);
 
+/* Stage timing for benchmarks: while enabled, every launch of a stage is
+ * bracketed by HIP events on the model's stream, and the stage's algorithmic
+ * work per launch (flops for GEMMs and attention, HBM bytes for the memory
+ * bound stages) is accumulated.  Enabling (on = 1) or disabling resets the
+ * counters.  dlmc_profile_read synchronises the stream and returns, for
+ * `stage` (DLMC_STAGE_*), the summed event time in ms, the number of
+ * launches and the summed work. */
+#define DLMC_STAGE_EMBED 0
+#define DLMC_STAGE_NORM 1
+#define DLMC_STAGE_QKV 2      /* QKV GEMM with rotary epilogue          */
+#define DLMC_STAGE_ATTN 3     /* non-causal flash attention             */
+#define DLMC_STAGE_OPROJ 4    /* O projection + residual                */
+#define DLMC_STAGE_FFN_IN 5   /* FFN in (GELU / SwiGLU gate+up)         */
+#define DLMC_STAGE_FFN_OUT 6  /* FFN out + residual                     */
+#define DLMC_STAGE_HEAD 7     /* LM head at masked rows                 */
+#define DLMC_STAGE_ENTROPY 8
+#define DLMC_STAGE_SELECT 9
+#define DLMC_STAGE_CDF 10
+#define DLMC_STAGE_REVEAL 11
+#define DLMC_STAGE_COMPACT 12
+#define DLMC_N_STAGES 13
+dlmc_status dlmc_profile_enable(dlmc_model* model, int32_t on);
+dlmc_status dlmc_profile_read(dlmc_model* model, int32_t stage, double* ms_total,
+                              uint64_t* launches, double* work);
+
 /* ---- host range coder hooks (no GPU needed) ----------------------------- */
 
 /* Range-code n symbol intervals [start_i, start_i + freq_i) of a 2^P total

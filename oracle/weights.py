@@ -18,6 +18,9 @@ ffn_out=6.  All tensors are [out_features, in_features]; the embedding is
 """
 from __future__ import annotations
 
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 
 MASK64 = (1 << 64) - 1
@@ -77,13 +80,23 @@ def gen_rows(seed: int, tensor_id: int, n_cols: int, rows: np.ndarray, exp: int,
 
 
 def gen_tensor(seed: int, tensor_id: int, shape, exp: int, dtype: str,
-               block_rows: int = 4096) -> np.ndarray:
-    """A whole [out, in] tensor (generated in row blocks to bound memory)."""
+               block_rows: int = 512) -> np.ndarray:
+    """A whole [out, in] tensor, generated in row blocks (bounded memory) on a
+    thread pool; every block is the same pure function of its row indices."""
     n_out, n_in = shape
     out = np.empty((n_out, n_in), dtype=np.float64)
-    for r0 in range(0, n_out, block_rows):
+
+    def fill(r0):
         r1 = min(n_out, r0 + block_rows)
         out[r0:r1] = gen_rows(seed, tensor_id, n_in, np.arange(r0, r1), exp, dtype)
+
+    starts = range(0, n_out, block_rows)
+    if n_out * n_in < (1 << 20):
+        for r0 in starts:
+            fill(r0)
+    else:
+        with ThreadPoolExecutor(min(16, os.cpu_count() or 1)) as ex:
+            list(ex.map(fill, starts))
     return out
 
 

@@ -24,6 +24,8 @@ FFN = {"gelu": 0, "swiglu": 1}
 NORM = {"layernorm": 0, "rmsnorm": 1}
 DTYPE = {"f32": 0, "bf16": 1}
 FLAG_CRC = 1
+STAGES = ["embed", "norm", "qkv", "attn", "oproj", "ffn_in", "ffn_out", "head", "entropy",
+          "select", "cdf", "reveal", "compact"]
 
 
 class LibraryMissing(RuntimeError):
@@ -80,6 +82,8 @@ _SIGS = {
     "dlmc_entropy_cdf": (i32, [vp, vp, i32, i32, vp, vp, vp, vp]),
     "dlmc_select": (i32, [vp, vp, vp, i32, i32, i32, f32, i32, i32, vp, vp, vp]),
     "dlmc_weight_copy": (i32, [vp, i32, vp, u64]),
+    "dlmc_profile_enable": (i32, [vp, i32]),
+    "dlmc_profile_read": (i32, [vp, i32, P(ctypes.c_double), P(u64), P(ctypes.c_double)]),
     "dlmc_rc_encode": (i32, [vp, vp, u64, i32, i32, vp, u64, P(u64)]),
     "dlmc_rc_decode": (i32, [vp, u64, vp, u64, i32, i32, i32, vp]),
     "dlmc_status_string": (ctypes.c_char_p, [i32]),
@@ -245,6 +249,20 @@ class Model:
 
         self._trace_cb = TRACE_FN(cb)
         _check(lib().dlmc_set_trace(self.handle, self._trace_cb, None))
+
+    def profile(self, on: bool):
+        """Enable / disable (and reset) per-stage event timing."""
+        _check(lib().dlmc_profile_enable(self.handle, 1 if on else 0))
+
+    def profile_read(self) -> dict:
+        """{stage: (ms_total, launches, work)} since profiling was enabled."""
+        out = {}
+        for i, name in enumerate(STAGES):
+            ms, n, wk = ctypes.c_double(0), u64(0), ctypes.c_double(0)
+            _check(lib().dlmc_profile_read(self.handle, i, ctypes.byref(ms), ctypes.byref(n),
+                                           ctypes.byref(wk)))
+            out[name] = (ms.value, n.value, wk.value)
+        return out
 
     def set_stream(self, stream_handle: Optional[int]):
         _check(lib().dlmc_set_stream(self.handle, stream_handle))

@@ -289,6 +289,26 @@ dlmc_status dlmc_weight_copy(dlmc_model* m, int32_t tensor_id, void* dst, uint64
   });
 }
 
+dlmc_status dlmc_profile_enable(dlmc_model* m, int32_t on) {
+  return guard([&] {
+    use(m);
+    m->prof_reset();
+    m->prof = on != 0;
+  });
+}
+
+dlmc_status dlmc_profile_read(dlmc_model* m, int32_t stage, double* ms_total, uint64_t* launches,
+                              double* work) {
+  return guard([&] {
+    use(m);
+    DLMC_CHECK(stage >= 0 && stage < DLMC_N_STAGES, DLMC_E_INVAL, "no such stage");
+    m->prof_collect();
+    if (ms_total) *ms_total = m->prof_ms[stage];
+    if (launches) *launches = m->prof_n[stage];
+    if (work) *work = m->prof_work[stage];
+  });
+}
+
 dlmc_status dlmc_rc_encode(const uint32_t* start, const uint32_t* freq, uint64_t n,
                            int32_t cdf_bits, int32_t coder_bits, uint8_t* out, uint64_t cap,
                            uint64_t* out_len) {

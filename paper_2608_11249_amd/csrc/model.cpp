@@ -10,6 +10,11 @@ using namespace dlmc;
 dlmc_model::~dlmc_model() {
   if (device >= 0) (void)hipSetDevice(device);
   if (stream) (void)hipStreamSynchronize(stream);
+  for (auto& r : prof_recs) {
+    (void)hipEventDestroy(r.a);
+    (void)hipEventDestroy(r.b);
+  }
+  for (hipEvent_t e : prof_pool) (void)hipEventDestroy(e);
   for (void* p : allocs) (void)hipFree(p);
   if (own_stream) (void)hipStreamDestroy(own_stream);
 }
@@ -62,6 +67,40 @@ void dlmc_model::ensure_tokens(size_t n) {
   dfree(tokens_dev);
   tokens_dev = (int32_t*)dalloc(std::max<size_t>(n, 1) * 4);
   tokens_cap = n;
+}
+
+hipEvent_t dlmc_model::prof_event() {
+  if (!prof_pool.empty()) {
+    hipEvent_t e = prof_pool.back();
+    prof_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e;
+  DLMC_HIP(hipEventCreate(&e));
+  return e;
+}
+
+void dlmc_model::prof_collect() {
+  if (prof_recs.empty()) return;
+  DLMC_HIP(hipStreamSynchronize(stream));
+  for (auto& r : prof_recs) {
+    float ms = 0.0f;
+    DLMC_HIP(hipEventElapsedTime(&ms, r.a, r.b));
+    prof_ms[r.stage] += ms;
+    prof_work[r.stage] += r.work;
+    prof_n[r.stage] += 1;
+    prof_pool.push_back(r.a);
+    prof_pool.push_back(r.b);
+  }
+  prof_recs.clear();
+}
+
+void dlmc_model::prof_reset() {
+  prof_collect();
+  for (int i = 0; i < DLMC_N_STAGES; ++i) {
+    prof_ms[i] = prof_work[i] = 0.0;
+    prof_n[i] = 0;
+  }
 }
 
 namespace dlmc {
@@ -228,7 +267,7 @@ uint64_t dlmc_model::hash() const {
 }
 
 void dlmc_model::forward(const int32_t* st_dev, int B, int T, float* logits_out, int32_t* rows_out,
-                         int32_t* n_rows_out) {
+                         int32_t* n_rows_out, int64_t rows_hint) {
   DLMC_CHECK(B >= 1 && B <= cfg.max_batch && T >= 1 && T <= cfg.max_chunk, DLMC_E_INVAL,
              "batch / chunk length exceed the model's workspace");
   const int d = cfg.d_model, F = cfg.d_ffn, V = cfg.vocab, H = cfg.n_heads;
@@ -239,8 +278,13 @@ void dlmc_model::forward(const int32_t* st_dev, int B, int T, float* logits_out,
   int32_t* rw = rows_out ? rows_out : rows;
   int32_t* nr = n_rows_out ? n_rows_out : n_rows;
   hipStream_t s = stream;
+  const double Md = M, dd = d, es = (double)esz;
+  const double head_rows = rows_hint >= 0 ? (double)rows_hint : Md;
 
-  dlmc::embed(s, st_dev, this->embed, cfg.dtype, x, M, d, V);
+  {
+    StageTimer t(this, DLMC_STAGE_EMBED, Md * dd * (es + 4.0));
+    dlmc::embed(s, st_dev, this->embed, cfg.dtype, x, M, d, V);
+  }
   EpiArgs qkv;
   qkv.q = q;
   qkv.k = k;
@@ -255,44 +299,88 @@ void dlmc_model::forward(const int32_t* st_dev, int B, int T, float* logits_out,
   EpiArgs resid;
   resid.out = x;
   resid.ldo = d;
+  const double norm_bytes = Md * dd * (4.0 + es);
   for (const Layer& w : layers) {
-    norm_rows(s, x, h, cfg.dtype, M, d, cfg.norm_kind, cfg.norm_eps, nullptr, nullptr);
-    if (bf16) {
-      gemm_bf16(s, (const bf16_t*)h, (const bf16_t*)w.wqkv, M, 3 * d, d, nullptr, EPI_QKV_ROPE, qkv);
-      attention_bf16(s, (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)vt, (bf16_t*)attn, B, H, T, Tp, dh);
-      gemm_bf16(s, (const bf16_t*)attn, (const bf16_t*)w.wo, M, d, d, nullptr, EPI_RESIDUAL, resid);
-    } else {
-      EpiArgs t;
-      t.out = tmp;
-      t.ldo = 3 * d;
-      gemm_f32(s, (const float*)h, (const float*)w.wqkv, M, 3 * d, d, nullptr, EPI_STORE_F32, t);
-      qkv_rope_f32(s, tmp, M, qkv);
-      attention_f32(s, (const float*)q, (const float*)k, (const float*)vt, (float*)attn, B, H, T, Tp, dh);
-      gemm_f32(s, (const float*)attn, (const float*)w.wo, M, d, d, nullptr, EPI_RESIDUAL, resid);
+    {
+      StageTimer t(this, DLMC_STAGE_NORM, norm_bytes);
+      norm_rows(s, x, h, cfg.dtype, M, d, cfg.norm_kind, cfg.norm_eps, nullptr, nullptr);
     }
-    norm_rows(s, x, h, cfg.dtype, M, d, cfg.norm_kind, cfg.norm_eps, nullptr, nullptr);
+    if (bf16) {
+      {
+        StageTimer t(this, DLMC_STAGE_QKV, 2.0 * Md * 3.0 * dd * dd);
+        gemm_bf16(s, (const bf16_t*)h, (const bf16_t*)w.wqkv, M, 3 * d, d, nullptr, EPI_QKV_ROPE, qkv);
+      }
+      {
+        StageTimer t(this, DLMC_STAGE_ATTN, 4.0 * B * H * (double)T * T * dh);
+        attention_bf16(s, (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)vt, (bf16_t*)attn, B, H, T, Tp, dh);
+      }
+      {
+        StageTimer t(this, DLMC_STAGE_OPROJ, 2.0 * Md * dd * dd);
+        gemm_bf16(s, (const bf16_t*)attn, (const bf16_t*)w.wo, M, d, d, nullptr, EPI_RESIDUAL, resid);
+      }
+    } else {
+      EpiArgs t3;
+      t3.out = tmp;
+      t3.ldo = 3 * d;
+      {
+        StageTimer t(this, DLMC_STAGE_QKV, 2.0 * Md * 3.0 * dd * dd);
+        gemm_f32(s, (const float*)h, (const float*)w.wqkv, M, 3 * d, d, nullptr, EPI_STORE_F32, t3);
+        qkv_rope_f32(s, tmp, M, qkv);
+      }
+      {
+        StageTimer t(this, DLMC_STAGE_ATTN, 4.0 * B * H * (double)T * T * dh);
+        attention_f32(s, (const float*)q, (const float*)k, (const float*)vt, (float*)attn, B, H, T, Tp, dh);
+      }
+      {
+        StageTimer t(this, DLMC_STAGE_OPROJ, 2.0 * Md * dd * dd);
+        gemm_f32(s, (const float*)attn, (const float*)w.wo, M, d, d, nullptr, EPI_RESIDUAL, resid);
+      }
+    }
+    {
+      StageTimer t(this, DLMC_STAGE_NORM, norm_bytes);
+      norm_rows(s, x, h, cfg.dtype, M, d, cfg.norm_kind, cfg.norm_eps, nullptr, nullptr);
+    }
     if (bf16) {
       EpiArgs f;
       f.out = ffn;
       f.ldo = F;
-      gemm_bf16(s, (const bf16_t*)h, (const bf16_t*)w.win, M, nF, d, nullptr,
-                glu ? EPI_SWIGLU : EPI_GELU, f);
-      gemm_bf16(s, (const bf16_t*)ffn, (const bf16_t*)w.wout, M, d, F, nullptr, EPI_RESIDUAL, resid);
+      {
+        StageTimer t(this, DLMC_STAGE_FFN_IN, 2.0 * Md * nF * dd);
+        gemm_bf16(s, (const bf16_t*)h, (const bf16_t*)w.win, M, nF, d, nullptr,
+                  glu ? EPI_SWIGLU : EPI_GELU, f);
+      }
+      {
+        StageTimer t(this, DLMC_STAGE_FFN_OUT, 2.0 * Md * dd * F);
+        gemm_bf16(s, (const bf16_t*)ffn, (const bf16_t*)w.wout, M, d, F, nullptr, EPI_RESIDUAL, resid);
+      }
     } else {
-      EpiArgs t;
-      t.out = tmp;
-      t.ldo = nF;
-      gemm_f32(s, (const float*)h, (const float*)w.win, M, nF, d, nullptr, EPI_STORE_F32, t);
-      ffn_act_f32(s, tmp, (float*)ffn, M, F, cfg.ffn_kind);
-      gemm_f32(s, (const float*)ffn, (const float*)w.wout, M, d, F, nullptr, EPI_RESIDUAL, resid);
+      EpiArgs t2;
+      t2.out = tmp;
+      t2.ldo = nF;
+      {
+        StageTimer t(this, DLMC_STAGE_FFN_IN, 2.0 * Md * nF * dd);
+        gemm_f32(s, (const float*)h, (const float*)w.win, M, nF, d, nullptr, EPI_STORE_F32, t2);
+        ffn_act_f32(s, tmp, (float*)ffn, M, F, cfg.ffn_kind);
+      }
+      {
+        StageTimer t(this, DLMC_STAGE_FFN_OUT, 2.0 * Md * dd * F);
+        gemm_f32(s, (const float*)ffn, (const float*)w.wout, M, d, F, nullptr, EPI_RESIDUAL, resid);
+      }
     }
   }
   // masked rows only: compaction, final norm gathered, LM head
-  compact_masked(s, st_dev, B, T, V, rw, nr, chunk_off, chunk_cnt);
-  norm_rows(s, x, hm, cfg.dtype, M, d, cfg.norm_kind, cfg.norm_eps, rw, nr);
+  {
+    StageTimer t(this, DLMC_STAGE_COMPACT, Md * 8.0);
+    compact_masked(s, st_dev, B, T, V, rw, nr, chunk_off, chunk_cnt);
+  }
+  {
+    StageTimer t(this, DLMC_STAGE_NORM, head_rows * dd * (4.0 + es));
+    norm_rows(s, x, hm, cfg.dtype, M, d, cfg.norm_kind, cfg.norm_eps, rw, nr);
+  }
   EpiArgs o;
   o.out = lg;
   o.ldo = V;
+  StageTimer t(this, DLMC_STAGE_HEAD, 2.0 * head_rows * V * dd);
   if (bf16)
     gemm_bf16(s, (const bf16_t*)hm, (const bf16_t*)this->head, M, V, d, nr, EPI_STORE_F32, o);
   else

@@ -53,6 +53,21 @@ struct dlmc_model {
   dlmc_trace_fn trace = nullptr;
   void* trace_user = nullptr;
 
+  // stage profiling (events bracket each stage launch while enabled)
+  struct ProfRec {
+    int stage;
+    hipEvent_t a, b;
+    double work;
+  };
+  bool prof = false;
+  std::vector<ProfRec> prof_recs;
+  std::vector<hipEvent_t> prof_pool;
+  double prof_ms[DLMC_N_STAGES] = {}, prof_work[DLMC_N_STAGES] = {};
+  uint64_t prof_n[DLMC_N_STAGES] = {};
+  hipEvent_t prof_event();
+  void prof_collect();
+  void prof_reset();
+
   ~dlmc_model();
   void* dalloc(size_t bytes, bool zero = false);
   void dfree(void* p);
@@ -62,8 +77,30 @@ struct dlmc_model {
   // One forward pass over state[B*T] (device): logits at masked rows into
   // logits_out (or the internal buffer), row ids and count likewise.
   void forward(const int32_t* state, int B, int T, float* logits_out, int32_t* rows_out,
-               int32_t* n_rows_out);
+               int32_t* n_rows_out, int64_t rows_hint = -1);
 };
+
+namespace dlmc {
+// Brackets one stage launch with events when the model's profiling is on.
+struct StageTimer {
+  dlmc_model* m;
+  int stage;
+  double work;
+  hipEvent_t a = nullptr;
+  StageTimer(dlmc_model* m_, int stage_, double work_) : m(m_), stage(stage_), work(work_) {
+    if (m->prof) {
+      a = m->prof_event();
+      DLMC_HIP(hipEventRecord(a, m->stream));
+    }
+  }
+  ~StageTimer() {
+    if (a) {
+      hipEvent_t b = m->prof_event();
+      if (hipEventRecord(b, m->stream) == hipSuccess) m->prof_recs.push_back({stage, a, b, work});
+    }
+  }
+};
+}  // namespace dlmc
 
 namespace dlmc {
 

@@ -126,20 +126,41 @@ int dlmc_session::step(uint64_t* coded) {
   }
   if (phase == 2) return 1;
 
-  m->forward(m->state, B, T, nullptr, nullptr, nullptr);
-  entropy_rows(s, m->logits, B * T, m->n_rows, V, m->H, m->mx);
-  select_positions(s, m->H, m->rows, m->chunk_off, m->chunk_cnt, B, T, cp.tau_bits, cp.m_min, mm,
-                   m->sel_pos, m->sel_row, m->n_sel, m->err);
-  cdf_rows(s, m->logits, m->mx, m->sel_row, m->n_sel, B, mm, V, P, m->cdf, nullptr);
-  if (encode)
+  int64_t masked = 0;  // masked positions before this pass (host bookkeeping)
+  for (int b = 0; b < B; ++b)
+    if (slot_chunk[b] >= 0) masked += slot_left[b];
+  m->forward(m->state, B, T, nullptr, nullptr, nullptr, masked);
+  {
+    StageTimer t(m, DLMC_STAGE_ENTROPY, (double)masked * V * 4.0);
+    entropy_rows(s, m->logits, B * T, m->n_rows, V, m->H, m->mx);
+  }
+  {
+    StageTimer t(m, DLMC_STAGE_SELECT, (double)masked * 8.0);
+    select_positions(s, m->H, m->rows, m->chunk_off, m->chunk_cnt, B, T, cp.tau_bits, cp.m_min, mm,
+                     m->sel_pos, m->sel_row, m->n_sel, m->err);
+  }
+  const size_t cdf_rec = m->prof_recs.size();
+  {
+    // work (read the row once, write the CDF) is filled in once n_sel is known
+    StageTimer t(m, DLMC_STAGE_CDF, 0.0);
+    cdf_rows(s, m->logits, m->mx, m->sel_row, m->n_sel, B, mm, V, P, m->cdf, nullptr);
+  }
+  if (encode) {
+    StageTimer t(m, DLMC_STAGE_REVEAL, 0.0);
     gather_reveal(s, m->cdf, m->sel_pos, m->n_sel, m->tokens_dev, m->slot_base, m->state, B, T, mm,
                   V, m->sym);
+  }
   DLMC_HIP(hipMemcpyAsync(h_nsel, m->n_sel, (size_t)B * 4, hipMemcpyDeviceToHost, s));
   DLMC_HIP(hipMemcpyAsync(h_pos, m->sel_pos, (size_t)B * mm * 4, hipMemcpyDeviceToHost, s));
   DLMC_HIP(hipMemcpyAsync(h_err, m->err, 4, hipMemcpyDeviceToHost, s));
   if (encode) DLMC_HIP(hipMemcpyAsync(h_sym, m->sym, (size_t)B * mm * 8, hipMemcpyDeviceToHost, s));
   DLMC_HIP(hipStreamSynchronize(s));
   if (*h_err) throw Error(DLMC_E_NUMERIC, "non-finite entropy (non-finite logits)");
+  if (m->prof && cdf_rec < m->prof_recs.size()) {
+    int64_t committed = 0;
+    for (int b = 0; b < B; ++b) committed += h_nsel[b];
+    m->prof_recs[cdf_rec].work = (double)committed * (8.0 * V + 4.0);
+  }
 
   const size_t row_words = (size_t)V + 1;
   std::vector<float> Hsel;
