@@ -191,16 +191,19 @@ dlmc_status dlmc_entropy_cdf(dlmc_model* m, const float* logits, int32_t n_rows,
       // every row committed: one "chunk" per row, n_sel = 1
       DLMC_CHECK(n_rows <= 65535, DLMC_E_INVAL, "at most 65535 CDF rows per call");
       int32_t *sel_row = nullptr, *n_sel = nullptr;
+      void* ws = nullptr;
       DLMC_HIP(hipMalloc((void**)&sel_row, (size_t)n_rows * 4));
       DLMC_HIP(hipMalloc((void**)&n_sel, (size_t)n_rows * 4));
+      DLMC_HIP(hipMalloc(&ws, cdf_workspace_bytes(n_rows, V)));
       std::vector<int32_t> idx(n_rows), one(n_rows, 1);
       for (int i = 0; i < n_rows; ++i) idx[i] = i;
       DLMC_HIP(hipMemcpyAsync(sel_row, idx.data(), idx.size() * 4, hipMemcpyHostToDevice, s));
       DLMC_HIP(hipMemcpyAsync(n_sel, one.data(), one.size() * 4, hipMemcpyHostToDevice, s));
-      cdf_rows(s, logits, row_max, sel_row, n_sel, n_rows, 1, V, cdf_bits, cdf, g);
+      cdf_rows(s, logits, row_max, sel_row, n_sel, n_rows, 1, V, cdf_bits, cdf, g, ws);
       DLMC_HIP(hipStreamSynchronize(s));
       (void)hipFree(sel_row);
       (void)hipFree(n_sel);
+      (void)hipFree(ws);
     }
     DLMC_HIP(hipStreamSynchronize(s));
   });

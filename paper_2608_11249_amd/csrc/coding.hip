@@ -228,58 +228,123 @@ __device__ __forceinline__ U block_sum_int(U v, U* red) {
   return red[0] + red[1] + red[2] + red[3];
 }
 
-// integer CDF of one committed row:
+// Integer CDF of the committed rows, each row split into CDF_SEG-entry
+// segments handled by separate workgroups (three passes):
 //   g_v = floor(exp(l_v - max) 2^24), G = sum g, f_v = 1 + floor(g_v (2^P - V) / G),
 //   the remainder 2^P - sum f goes to the lowest index of maximal g,
 //   cdf[0] = 0, cdf[v+1] = cdf[v] + f_v.
-__global__ void __launch_bounds__(256)
-cdf_kernel(const float* __restrict__ logits, const float* __restrict__ mx,
-           const int32_t* __restrict__ sel_row, const int32_t* __restrict__ n_sel, int m_max,
-           int V, int P, uint32_t* __restrict__ cdf, uint32_t* __restrict__ g_out) {
+// Pass A: per-segment sum of g and lowest index with g = 2^24; pass B:
+// per-segment sum of f; pass C: segment offset + in-segment scan.  Every sum
+// is an integer, so the segment split does not change a single bit.
+constexpr int CDF_SEG = 4096;
+
+struct CdfArgs {
+  const float* logits;
+  const float* mx;
+  const int32_t* sel_row;
+  const int32_t* n_sel;
+  int m_max, V, P, S;
+  uint32_t* cdf;
+  uint32_t* g_out;
+  uint64_t* segG;
+  uint64_t* segF;
+  int32_t* segA;
+};
+
+__global__ void __launch_bounds__(256) cdf_pass_a(CdfArgs c) {
   __shared__ uint64_t red64[4];
   __shared__ int redi[4];
-  __shared__ uint32_t scan[4];
-  const int j = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  if (j >= n_sel[b]) return;
-  const int slot = b * m_max + j;
-  const int row = sel_row[slot];
-  const float* lg = logits + (size_t)row * V;
-  const float m = mx[row];
-  uint32_t* out = cdf + (size_t)slot * (V + 1);
-
+  const int seg = blockIdx.x, slot = blockIdx.y, b = slot / c.m_max, j = slot % c.m_max;
+  if (j >= c.n_sel[b]) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int row = c.sel_row[slot];
+  const float* lg = c.logits + (size_t)row * c.V;
+  const float m = c.mx[row];
+  const int v0 = seg * CDF_SEG, v1 = min(c.V, v0 + CDF_SEG);
   uint64_t G = 0;
   int a = INT_MAX;
-  for (int v = tid; v < V; v += 256) {
+  for (int v = v0 + tid; v < v1; v += 256) {
     const uint32_t g = gval(lg[v], m);
     G += g;
     if (g == (1u << 24)) a = min(a, v);
-    if (g_out) g_out[(size_t)slot * V + v] = g;
+    if (c.g_out) c.g_out[(size_t)slot * c.V + v] = g;
   }
   G = block_sum_int<uint64_t>(G, red64);
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) a = min(a, __shfl_xor(a, o));
   if (lane == 0) redi[wave] = a;
   __syncthreads();
-  a = min(min(redi[0], redi[1]), min(redi[2], redi[3]));
+  if (tid == 0) {
+    c.segG[(size_t)slot * c.S + seg] = G;
+    c.segA[(size_t)slot * c.S + seg] = min(min(redi[0], redi[1]), min(redi[2], redi[3]));
+  }
+}
 
-  const uint64_t c = (1ull << P) - (uint64_t)V;
+__device__ __forceinline__ uint64_t row_G(const CdfArgs& c, int slot) {
+  uint64_t G = 0;
+  for (int s = 0; s < c.S; ++s) G += c.segG[(size_t)slot * c.S + s];
+  return G;
+}
+
+__global__ void __launch_bounds__(256) cdf_pass_b(CdfArgs c) {
+  __shared__ uint64_t red64[4];
+  __shared__ uint64_t sG;
+  const int seg = blockIdx.x, slot = blockIdx.y, b = slot / c.m_max, j = slot % c.m_max;
+  if (j >= c.n_sel[b]) return;
+  const int tid = threadIdx.x;
+  if (tid == 0) sG = row_G(c, slot);
+  __syncthreads();
+  const uint64_t G = sG, cst = (1ull << c.P) - (uint64_t)c.V;
+  const int row = c.sel_row[slot];
+  const float* lg = c.logits + (size_t)row * c.V;
+  const float m = c.mx[row];
+  const int v0 = seg * CDF_SEG, v1 = min(c.V, v0 + CDF_SEG);
   uint64_t F = 0;
-  for (int v = tid; v < V; v += 256) F += 1 + (uint64_t)gval(lg[v], m) * c / G;
+  for (int v = v0 + tid; v < v1; v += 256) F += 1 + (uint64_t)gval(lg[v], m) * cst / G;
   F = block_sum_int<uint64_t>(F, red64);
-  const uint32_t R = (uint32_t)((1ull << P) - F);
+  if (tid == 0) c.segF[(size_t)slot * c.S + seg] = F;
+}
 
-  if (tid == 0) out[0] = 0;
-  uint32_t carry = 0;
-  for (int base = 0; base < V; base += 1024) {
-    const int v0 = base + tid * 4;
+__global__ void __launch_bounds__(256) cdf_pass_c(CdfArgs c) {
+  __shared__ uint64_t sh[3];
+  __shared__ uint32_t scan[4];
+  const int seg = blockIdx.x, slot = blockIdx.y, b = slot / c.m_max, j = slot % c.m_max;
+  if (j >= c.n_sel[b]) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (tid == 0) {
+    uint64_t F = 0, before = 0;
+    int a = INT_MAX;
+    for (int s = 0; s < c.S; ++s) {
+      const uint64_t f = c.segF[(size_t)slot * c.S + s];
+      F += f;
+      if (s < seg) before += f;
+      a = min(a, c.segA[(size_t)slot * c.S + s]);
+    }
+    const uint64_t R = (1ull << c.P) - F;
+    sh[0] = row_G(c, slot);
+    sh[1] = before + ((a < seg * CDF_SEG) ? R : 0);  // cdf value entering this segment
+    sh[2] = ((uint64_t)(uint32_t)a << 32) | (uint32_t)R;
+  }
+  __syncthreads();
+  const uint64_t G = sh[0], cst = (1ull << c.P) - (uint64_t)c.V;
+  const int a = (int)(sh[2] >> 32);
+  const uint32_t R = (uint32_t)(sh[2] & 0xFFFFFFFFu);
+  const int row = c.sel_row[slot];
+  const float* lg = c.logits + (size_t)row * c.V;
+  const float m = c.mx[row];
+  uint32_t* out = c.cdf + (size_t)slot * (c.V + 1);
+  if (seg == 0 && tid == 0) out[0] = 0;
+  const int v0 = seg * CDF_SEG, v1 = min(c.V, v0 + CDF_SEG);
+  uint32_t carry = (uint32_t)sh[1];
+  for (int base = v0; base < v1; base += 1024) {
+    const int w0 = base + tid * 4;
     uint32_t f[4], loc = 0;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const int v = v0 + e;
-      f[e] = v < V ? 1u + (uint32_t)((uint64_t)gval(lg[v], m) * c / G) + (v == a ? R : 0u) : 0u;
+      const int v = w0 + e;
+      f[e] = v < v1 ? 1u + (uint32_t)((uint64_t)gval(lg[v], m) * cst / G) + (v == a ? R : 0u) : 0u;
       loc += f[e];
     }
-    // exclusive scan of loc over the block (integer: order-free)
     uint32_t inc = loc;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
@@ -294,8 +359,8 @@ cdf_kernel(const float* __restrict__ logits, const float* __restrict__ mx,
     uint32_t run = carry + wpre + inc - loc;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const int v = v0 + e;
-      if (v < V) {
+      const int v = w0 + e;
+      if (v < v1) {
         run += f[e];
         out[v + 1] = run;
       }
@@ -358,13 +423,33 @@ void select_positions(hipStream_t st, const float* H, const int32_t* rows,
   DLMC_HIP(hipGetLastError());
 }
 
+int cdf_segments(int V) { return ceil_div(V, CDF_SEG); }
+
 void cdf_rows(hipStream_t st, const float* logits, const float* mx, const int32_t* sel_row,
               const int32_t* n_sel, int B, int m_max, int V, int P, uint32_t* cdf,
-              uint32_t* g_out) {
+              uint32_t* g_out, void* seg_ws) {
   if (B <= 0) return;
   DLMC_CHECK(P <= 31 && (1ll << P) > V, DLMC_E_INVAL, "CDF precision must exceed the alphabet");
-  dim3 grid(m_max, B);
-  cdf_kernel<<<grid, 256, 0, st>>>(logits, mx, sel_row, n_sel, m_max, V, P, cdf, g_out);
+  DLMC_CHECK((int64_t)B * m_max <= 65535, DLMC_E_INVAL, "too many CDF rows per launch");
+  CdfArgs c;
+  c.logits = logits;
+  c.mx = mx;
+  c.sel_row = sel_row;
+  c.n_sel = n_sel;
+  c.m_max = m_max;
+  c.V = V;
+  c.P = P;
+  c.S = cdf_segments(V);
+  c.cdf = cdf;
+  c.g_out = g_out;
+  const size_t n = (size_t)B * m_max * c.S;
+  c.segG = (uint64_t*)seg_ws;
+  c.segF = c.segG + n;
+  c.segA = (int32_t*)(c.segF + n);
+  dim3 grid(c.S, B * m_max);
+  cdf_pass_a<<<grid, 256, 0, st>>>(c);
+  cdf_pass_b<<<grid, 256, 0, st>>>(c);
+  cdf_pass_c<<<grid, 256, 0, st>>>(c);
   DLMC_HIP(hipGetLastError());
 }
 

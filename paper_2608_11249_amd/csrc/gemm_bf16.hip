@@ -3,10 +3,16 @@
 // Every dense contraction of the forward pass (QKV, O, FFN in/out, LM head)
 // runs here.  Block tile BM x BN x 64 with four 64-wide waves in a 2 x 2
 // grid; each wave owns a (BM/2) x (BN/2) sub-tile built from
-// v_mfma_f32_32x32x16_bf16 tiles.  Global -> register -> LDS staging is double
-// buffered (one barrier per k-tile).  LDS rows are 64 bf16 (128 B); the eight
-// 16-byte chunks of row r are stored XOR-swizzled by (r & 7) so the
-// ds_read_b128 fragment loads of 8 consecutive rows hit 8 distinct bank groups.
+// v_mfma_f32_32x32x16_bf16 tiles.  Operand tiles move global -> LDS with
+// direct loads (global_load_lds_dwordx4) into a double-buffered LDS tile, one
+// barrier per k-tile.  LDS rows are 64 bf16 (128 B); the eight 16-byte chunks
+// of row r are XOR-swizzled by (r & 7) so the ds_read_b128 fragment loads of
+// 8 consecutive rows hit 8 distinct bank groups.  The fragment reads of k step
+// s + 1 are scheduled between the MFMAs of step s.
+//
+// Measured on MI355X (M = 2048): the fill of LDS from L2 (about 44 B/clk/CU at
+// best, latency-bound per CU) limits these shapes, so 128 x 128 tiles with two
+// blocks per CU win for the forward GEMMs; 256 x 256 wins for the LM head.
 //
 // Numerics: each output element is a sequential sum over k-tiles, each k-tile
 // four MFMA steps in order, independent of the tile shape and of which other
@@ -23,111 +29,14 @@ __device__ __forceinline__ float gelu_erf(float v) {
 }
 __device__ __forceinline__ float silu(float v) { return v / (1.0f + expf(-v)); }
 
+// acc[i][j][r] holds C[row][col] with row = i*32 + (r/4)*8 + lg*4 + r%4 and
+// col = j*32 + lr inside the wave tile of wave (wm, wn).
 template <int BM, int BN, int EPI>
-__global__ void __launch_bounds__(256)
-gemm_bf16_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, int M, int N,
-                 int K, const int* __restrict__ M_dev, EpiArgs ea, int n_tm) {
+__device__ __forceinline__ void epilogue(f32x16 (&acc)[BM / 64][BN / 64], int m0, int n0, int wm,
+                                         int wn, int lane, int Mv, int N, const EpiArgs& ea) {
   constexpr int WM = BM / 2, WN = BN / 2;
   constexpr int TM = WM / 32, TN = WN / 32;
-  constexpr int A_CH = BM * BK / 8 / 256;  // 16-byte chunks per thread per k-tile
-  constexpr int B_CH = BN * BK / 8 / 256;
-  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * (BM + BN) * BK];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int Mv = M_dev ? min(*M_dev, M) : M;
-
-  // XCD-aware remap: consecutive hardware block ids land on different XCDs
-  // (round robin over 8); give each XCD a contiguous range of logical tiles
-  // so tiles that share an operand panel share an L2.
-  int bid = blockIdx.x;
-  const int nb = gridDim.x;
-  if ((nb & 7) == 0) bid = (bid & 7) * (nb >> 3) + (bid >> 3);
-  const int tm = bid % n_tm, tn = bid / n_tm;
-  const int m0 = tm * BM, n0 = tn * BN;
-  if (m0 >= Mv) return;
-
-  bf16_t* As = smem;
-  bf16_t* Bs = smem + 2 * BM * BK;
-
-  // This thread's 16-byte chunks: rows row0 + 32 j (j < A_CH / B_CH) of the
-  // tile, 8-element column chunk kc; the swizzle depends on row & 7 only, so
-  // every chunk of the thread shares it.
-  const int row0 = tid >> 3, kc0 = tid & 7;
-  const int sw = (kc0 ^ (row0 & 7)) << 3;
-  int a_off[A_CH], b_off[B_CH];  // element offsets (< 2^31, checked on the host)
-#pragma unroll
-  for (int j = 0; j < A_CH; ++j) a_off[j] = min(m0 + row0 + 32 * j, Mv - 1) * K + kc0 * 8;
-#pragma unroll
-  for (int j = 0; j < B_CH; ++j) b_off[j] = min(n0 + row0 + 32 * j, N - 1) * K + kc0 * 8;
-  const int lds0 = row0 * BK + sw;
-
   const int lr = lane & 31, lg = lane >> 5;
-  u32x4 ra[A_CH], rb[B_CH];
-  f32x16 acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
-
-  const int nk = K / BK;
-#pragma unroll
-  for (int j = 0; j < A_CH; ++j) ra[j] = *reinterpret_cast<const u32x4*>(A + a_off[j]);
-#pragma unroll
-  for (int j = 0; j < B_CH; ++j) rb[j] = *reinterpret_cast<const u32x4*>(Bw + b_off[j]);
-#pragma unroll
-  for (int j = 0; j < A_CH; ++j) *reinterpret_cast<u32x4*>(As + lds0 + 32 * j * BK) = ra[j];
-#pragma unroll
-  for (int j = 0; j < B_CH; ++j) *reinterpret_cast<u32x4*>(Bs + lds0 + 32 * j * BK) = rb[j];
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    const bool more = kt + 1 < nk;
-    if (more) {
-      const int k1 = (kt + 1) * BK;
-#pragma unroll
-      for (int j = 0; j < A_CH; ++j) ra[j] = *reinterpret_cast<const u32x4*>(A + a_off[j] + k1);
-#pragma unroll
-      for (int j = 0; j < B_CH; ++j) rb[j] = *reinterpret_cast<const u32x4*>(Bw + b_off[j] + k1);
-    }
-    const bf16_t* as = As + cur * BM * BK;
-    const bf16_t* bs = Bs + cur * BN * BK;
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      const int kc = ks * 2 + lg;
-      bf16x8 af[TM], bfr[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        const int row = wm * WM + i * 32 + lr;
-        af[i] = *reinterpret_cast<const bf16x8*>(as + row * BK + ((kc ^ (row & 7)) << 3));
-      }
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int row = wn * WN + j * 32 + lr;
-        bfr[j] = *reinterpret_cast<const bf16x8*>(bs + row * BK + ((kc ^ (row & 7)) << 3));
-      }
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-    }
-    if (more) {
-      bf16_t* an = As + (cur ^ 1) * BM * BK;
-      bf16_t* bn = Bs + (cur ^ 1) * BN * BK;
-#pragma unroll
-      for (int j = 0; j < A_CH; ++j) *reinterpret_cast<u32x4*>(an + lds0 + 32 * j * BK) = ra[j];
-#pragma unroll
-      for (int j = 0; j < B_CH; ++j) *reinterpret_cast<u32x4*>(bn + lds0 + 32 * j * BK) = rb[j];
-    }
-    __syncthreads();
-  }
-
-  // ---------------------------------------------------------------- epilogue
-  // acc[i][j][r] holds C[row][col] with row = i*32 + (r/4)*8 + lg*4 + r%4 and
-  // col = j*32 + lr inside the wave tile.
   const int wrow0 = m0 + wm * WM, wcol0 = n0 + wn * WN;
   if constexpr (EPI == EPI_QKV_ROPE) {
     const int d = ea.d, dh = ea.dh, T = ea.T, Tp = ea.Tp, H = ea.H, half = dh / 2;
@@ -197,55 +106,195 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, in
   }
 }
 
+// 16-byte direct global -> LDS load (global_load_lds_dwordx4).  `lds` must be
+// wave-uniform: lane l writes lds + 16 l bytes.  The builtin exists only for
+// the device target, so the host pass sees an empty body.
+__device__ __forceinline__ void lds_dma16(const bf16_t* g, bf16_t* lds) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_global_load_lds(g, lds, 16, 0, 0);
+#endif
+}
+
+// MFMA fragment loads of one 16-deep k step: rows w0 + 32 i + lr, 16-byte
+// chunk kc of each 128-byte LDS row (XOR-swizzled by row & 7).
+template <int NT>
+__device__ __forceinline__ void load_frags(bf16x8 (&f)[NT], const bf16_t* base, int w0, int lr,
+                                           int kc) {
+#pragma unroll
+  for (int i = 0; i < NT; ++i) {
+    const int row = w0 + i * 32 + lr;
+    f[i] = *reinterpret_cast<const bf16x8*>(base + row * BK + ((kc ^ (row & 7)) << 3));
+  }
+}
+
+template <int TM, int TN>
+__device__ __forceinline__ void mfma_block(f32x16 (&acc)[TM][TN], const bf16x8 (&a)[TM],
+                                           const bf16x8 (&b)[TN]) {
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+}
+
+// Each wave load instruction fills one contiguous 1 KB LDS window (8 tile
+// rows); the XOR swizzle is applied on the global side, lane l of the window
+// fetching chunk (l & 7) ^ (row & 7) of its row.  No VGPR staging, no
+// ds_write.  MFMA fragments are double buffered in registers across the four
+// k steps.
+template <int BM, int BN, int EPI>
+__global__ void __launch_bounds__(256)
+gemm_bf16_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, int M, int N,
+                 int K, const int* __restrict__ M_dev, EpiArgs ea, int n_tm) {
+  constexpr int WM = BM / 2, WN = BN / 2;
+  constexpr int TM = WM / 32, TN = WN / 32;
+  constexpr int A_IN = BM / 32;  // 1 KB load instructions per wave per k-tile
+  constexpr int B_IN = BN / 32;
+  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * (BM + BN) * BK];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int lr = lane & 31, lg = lane >> 5;
+  const int Mv = M_dev ? min(*M_dev, M) : M;
+  int bid = blockIdx.x;
+  const int nb = gridDim.x;
+  if ((nb & 7) == 0) bid = (bid & 7) * (nb >> 3) + (bid >> 3);
+  const int tm = bid % n_tm, tn = bid / n_tm;
+  const int m0 = tm * BM, n0 = tn * BN;
+  if (m0 >= Mv) return;
+
+  bf16_t* As = smem;
+  bf16_t* Bs = smem + 2 * BM * BK;
+  int a_off[A_IN], b_off[B_IN];
+#pragma unroll
+  for (int j = 0; j < A_IN; ++j) {
+    const int sl = (wave * A_IN + j) * 64 + lane, row = sl >> 3;
+    a_off[j] = min(m0 + row, Mv - 1) * K + (((sl & 7) ^ (row & 7)) << 3);
+  }
+#pragma unroll
+  for (int j = 0; j < B_IN; ++j) {
+    const int sl = (wave * B_IN + j) * 64 + lane, row = sl >> 3;
+    b_off[j] = min(n0 + row, N - 1) * K + (((sl & 7) ^ (row & 7)) << 3);
+  }
+  const int a_win = wave * A_IN * 512, b_win = wave * B_IN * 512;  // this wave's LDS windows
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  const int nk = K / BK;
+#pragma unroll
+  for (int j = 0; j < A_IN; ++j)
+    lds_dma16(A + a_off[j], As + a_win + j * 512);
+#pragma unroll
+  for (int j = 0; j < B_IN; ++j)
+    lds_dma16(Bw + b_off[j], Bs + b_win + j * 512);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < nk) {
+      const int k1 = (kt + 1) * BK;
+      bf16_t* an = As + (cur ^ 1) * BM * BK + a_win;
+      bf16_t* bn = Bs + (cur ^ 1) * BN * BK + b_win;
+#pragma unroll
+      for (int j = 0; j < A_IN; ++j)
+        lds_dma16(A + a_off[j] + k1, an + j * 512);
+#pragma unroll
+      for (int j = 0; j < B_IN; ++j)
+        lds_dma16(Bw + b_off[j] + k1, bn + j * 512);
+    }
+    const bf16_t* as = As + cur * BM * BK;
+    const bf16_t* bs = Bs + cur * BN * BK;
+    bf16x8 a0[TM], b0[TN], a1[TM], b1[TN];
+    load_frags<TM>(a0, as, wm * WM, lr, lg);
+    load_frags<TN>(b0, bs, wn * WN, lr, lg);
+    load_frags<TM>(a1, as, wm * WM, lr, 2 + lg);
+    load_frags<TN>(b1, bs, wn * WN, lr, 2 + lg);
+    mfma_block<TM, TN>(acc, a0, b0);
+    load_frags<TM>(a0, as, wm * WM, lr, 4 + lg);
+    load_frags<TN>(b0, bs, wn * WN, lr, 4 + lg);
+    mfma_block<TM, TN>(acc, a1, b1);
+    load_frags<TM>(a1, as, wm * WM, lr, 6 + lg);
+    load_frags<TN>(b1, bs, wn * WN, lr, 6 + lg);
+    mfma_block<TM, TN>(acc, a0, b0);
+    mfma_block<TM, TN>(acc, a1, b1);
+    {
+      // software pipeline: the DS reads of k step s+1 and the direct loads of
+      // the next k-tile are spread between the MFMAs of k step s
+      constexpr int NF = TM + TN, NM = TM * TN, NV = A_IN + B_IN;
+      __builtin_amdgcn_sched_group_barrier(0x100, NF, 0);
+#pragma unroll
+      for (int i = 0; i < NF; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        if (i < NV) __builtin_amdgcn_sched_group_barrier(0x020, NV / NF > 0 ? NV / NF : 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, NM / NF, 0);
+      }
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+        for (int i = 0; i < NF; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, NM / NF, 0);
+        }
+      __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+  }
+  epilogue<BM, BN, EPI>(acc, m0, n0, wm, wn, lane, Mv, N, ea);
+}
+
+template <int BM, int BN, int EPI>
+void launch_epi(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int K,
+                const int* M_dev, const EpiArgs& ea) {
+  const int n_tm = ceil_div(M, BM), n_tn = ceil_div(N, BN);
+  gemm_bf16_kernel<BM, BN, EPI><<<dim3(n_tm * n_tn), dim3(256), 0, st>>>(A, B, M, N, K, M_dev, ea, n_tm);
+  DLMC_HIP(hipGetLastError());
+}
+
 template <int BM, int BN>
 void launch(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int K,
             const int* M_dev, EpiKind epi, const EpiArgs& ea) {
-  const int n_tm = ceil_div(M, BM), n_tn = ceil_div(N, BN);
-  dim3 grid(n_tm * n_tn), block(256);
   switch (epi) {
-    case EPI_STORE_F32:
-      gemm_bf16_kernel<BM, BN, EPI_STORE_F32><<<grid, block, 0, st>>>(A, B, M, N, K, M_dev, ea, n_tm);
-      break;
-    case EPI_RESIDUAL:
-      gemm_bf16_kernel<BM, BN, EPI_RESIDUAL><<<grid, block, 0, st>>>(A, B, M, N, K, M_dev, ea, n_tm);
-      break;
-    case EPI_GELU:
-      gemm_bf16_kernel<BM, BN, EPI_GELU><<<grid, block, 0, st>>>(A, B, M, N, K, M_dev, ea, n_tm);
-      break;
+    case EPI_STORE_F32: launch_epi<BM, BN, EPI_STORE_F32>(st, A, B, M, N, K, M_dev, ea); break;
+    case EPI_RESIDUAL: launch_epi<BM, BN, EPI_RESIDUAL>(st, A, B, M, N, K, M_dev, ea); break;
+    case EPI_GELU: launch_epi<BM, BN, EPI_GELU>(st, A, B, M, N, K, M_dev, ea); break;
     case EPI_QKV_ROPE:
     case EPI_SWIGLU:
       if constexpr (BN == 256) {
         throw Error(DLMC_E_INVAL, "paired epilogues use BN = 128");
       } else if (epi == EPI_QKV_ROPE) {
-        gemm_bf16_kernel<BM, BN, EPI_QKV_ROPE><<<grid, block, 0, st>>>(A, B, M, N, K, M_dev, ea, n_tm);
+        launch_epi<BM, BN, EPI_QKV_ROPE>(st, A, B, M, N, K, M_dev, ea);
       } else {
-        gemm_bf16_kernel<BM, BN, EPI_SWIGLU><<<grid, block, 0, st>>>(A, B, M, N, K, M_dev, ea, n_tm);
+        launch_epi<BM, BN, EPI_SWIGLU>(st, A, B, M, N, K, M_dev, ea);
       }
       break;
   }
-  DLMC_HIP(hipGetLastError());
 }
 
 }  // namespace
 
 void gemm_bf16(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int K,
-               const int* M_dev, EpiKind epi, const EpiArgs& ea) {
+               const int* M_dev, EpiKind epi, const EpiArgs& ea, int rows_hint) {
   DLMC_CHECK(K % BK == 0 && K > 0, DLMC_E_INVAL, "bf16 GEMM needs K % 64 == 0");
   DLMC_CHECK((int64_t)M * K < (1ll << 31) && (int64_t)N * K < (1ll << 31), DLMC_E_INVAL,
              "GEMM operand too large for 32-bit offsets");
   if (M <= 0 || N <= 0) return;
   const bool paired = (epi == EPI_QKV_ROPE || epi == EPI_SWIGLU);
-  // Tile choice: large tiles when there are enough of them to fill 256 CUs.
-  const long tiles256 = (long)ceil_div(M, 256) * ceil_div(N, 256);
-  // (the paired epilogues keep 2 x 256 accumulators live and spill at 256 x 256)
-  if (!paired && N % 256 == 0 && M >= 256 && tiles256 >= 512) {
+  DLMC_CHECK(!paired || N % 128 == 0, DLMC_E_INVAL, "paired epilogue needs N % 128 == 0");
+  // Tile choice (never changes the result): 256 x 256 for the fp32-store
+  // (LM head) when enough rows are live, 128 x 128 otherwise.
+  const int live = rows_hint >= 0 ? std::min(rows_hint, M) : M;
+  if (epi == EPI_STORE_F32 && N % 256 == 0 && live >= 512)
     launch<256, 256>(st, A, B, M, N, K, M_dev, epi, ea);
-  } else if ((!paired || N % 128 == 0) && M >= 128 && (long)ceil_div(M, 256) * ceil_div(N, 128) >= 256) {
-    launch<256, 128>(st, A, B, M, N, K, M_dev, epi, ea);
-  } else {
-    DLMC_CHECK(!paired || N % 128 == 0, DLMC_E_INVAL, "paired epilogue needs N % 128 == 0");
+  else
     launch<128, 128>(st, A, B, M, N, K, M_dev, epi, ea);
-  }
 }
 
 }  // namespace dlmc

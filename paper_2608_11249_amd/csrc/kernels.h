@@ -28,9 +28,10 @@ struct EpiArgs {
 };
 
 // M_dev (optional): device int holding the live row count (<= M); rows at or
-// beyond it are neither computed (whole tiles) nor stored.
+// beyond it are neither computed (whole tiles) nor stored.  rows_hint: the
+// live row count if the host knows it (tile selection only), else -1.
 void gemm_bf16(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int K,
-               const int* M_dev, EpiKind epi, const EpiArgs& ea);
+               const int* M_dev, EpiKind epi, const EpiArgs& ea, int rows_hint = -1);
 void gemm_f32(hipStream_t st, const float* A, const float* B, int M, int N, int K,
               const int* M_dev, EpiKind epi, const EpiArgs& ea);
 
@@ -78,9 +79,14 @@ void select_positions(hipStream_t st, const float* H, const int32_t* rows,
                       int32_t* n_sel, int32_t* err_flag);
 // integer CDF of row sel_row[b*m_max+j] of logits (for j < n_sel[b]) into
 // cdf[(b*m_max+j)*(V+1) ..]; g_out (optional) receives the g values.
+// seg_ws: device workspace of cdf_workspace_bytes(B * m_max, V) bytes.
+int cdf_segments(int V);
+inline size_t cdf_workspace_bytes(size_t slots, int V) {
+  return slots * (size_t)cdf_segments(V) * (8 + 8 + 4);
+}
 void cdf_rows(hipStream_t st, const float* logits, const float* mx, const int32_t* sel_row,
               const int32_t* n_sel, int B, int m_max, int V, int P, uint32_t* cdf,
-              uint32_t* g_out);
+              uint32_t* g_out, void* seg_ws);
 // encode: (start, freq) of the true symbol of every committed position and reveal it
 void gather_reveal(hipStream_t st, const uint32_t* cdf, const int32_t* sel_pos,
                    const int32_t* n_sel, const int32_t* tokens, const int64_t* slot_base,

@@ -51,6 +51,7 @@ void dlmc_model::ensure_sel(int m_max) {
   dfree(cdf);
   dfree(sym);
   dfree(slot_base);
+  dfree(cdf_ws);
   const size_t slots = (size_t)cfg.max_batch * m_max;
   sel_pos = (int32_t*)dalloc(slots * 4, true);
   sel_row = (int32_t*)dalloc(slots * 4, true);
@@ -59,6 +60,7 @@ void dlmc_model::ensure_sel(int m_max) {
   cdf = (uint32_t*)dalloc(slots * (size_t)(cfg.vocab + 1) * 4);
   sym = (uint32_t*)dalloc(slots * 8, true);
   slot_base = (int64_t*)dalloc((size_t)cfg.max_batch * 8, true);
+  cdf_ws = dalloc(cdf_workspace_bytes(slots, cfg.vocab));
   sel_cap = m_max;
 }
 
@@ -382,7 +384,8 @@ void dlmc_model::forward(const int32_t* st_dev, int B, int T, float* logits_out,
   o.ldo = V;
   StageTimer t(this, DLMC_STAGE_HEAD, 2.0 * head_rows * V * dd);
   if (bf16)
-    gemm_bf16(s, (const bf16_t*)hm, (const bf16_t*)this->head, M, V, d, nr, EPI_STORE_F32, o);
+    gemm_bf16(s, (const bf16_t*)hm, (const bf16_t*)this->head, M, V, d, nr, EPI_STORE_F32, o,
+              rows_hint >= 0 ? (int)rows_hint : -1);
   else
     gemm_f32(s, (const float*)hm, (const float*)this->head, M, V, d, nr, EPI_STORE_F32, o);
 }

@@ -46,6 +46,7 @@ struct dlmc_model {
   int sel_cap = 0;
   int32_t *sel_pos = nullptr, *sel_row = nullptr, *n_sel = nullptr, *dec = nullptr;
   uint32_t *cdf = nullptr, *sym = nullptr;
+  void* cdf_ws = nullptr;  // segment partials of the CDF kernels
   int64_t* slot_base = nullptr;
   int32_t* tokens_dev = nullptr;
   size_t tokens_cap = 0;

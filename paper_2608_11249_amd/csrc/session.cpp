@@ -143,7 +143,7 @@ int dlmc_session::step(uint64_t* coded) {
   {
     // work (read the row once, write the CDF) is filled in once n_sel is known
     StageTimer t(m, DLMC_STAGE_CDF, 0.0);
-    cdf_rows(s, m->logits, m->mx, m->sel_row, m->n_sel, B, mm, V, P, m->cdf, nullptr);
+    cdf_rows(s, m->logits, m->mx, m->sel_row, m->n_sel, B, mm, V, P, m->cdf, nullptr, m->cdf_ws);
   }
   if (encode) {
     StageTimer t(m, DLMC_STAGE_REVEAL, 0.0);
