@@ -1,0 +1,124 @@
+"""GPU checks of the five workload configurations at their real model shapes.
+
+Round trips use a prefix of each workload's seeded stream (whole chunks, in
+the workload's chunk length and schedule); batch sizes are reduced where a
+full batch would not fit a test's time budget -- the kernels are batch
+invariant, which test_gpu_parity checks separately.  Logits of the 8B-shaped
+model are compared with the oracle at full width with one layer (the launch
+shapes of every kernel are those of the 32-layer model), on a sample of
+vocabulary columns.
+"""
+import dataclasses
+import time
+
+import numpy as np
+import pytest
+
+import workloads as wl
+from oracle import model as OM
+from oracle import weights as OW
+
+from gpu_common import log, payloads, rel_err_rows, shape
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+import paper_2608_11249_amd as dl  # noqa: E402
+
+
+def dev_state(st):
+    return torch.from_numpy(np.ascontiguousarray(st, dtype=np.int32)).cuda()
+
+
+def roundtrip_workload(name, n_chunks, batch=None, max_seconds=None):
+    w = wl.WORKLOADS[name]
+    cd = w.codec if batch is None else dataclasses.replace(w.codec, batch=batch)
+    toks = wl.make_tokens(w, n_chunks * cd.chunk_len)
+    log("round trip", name, f"{n_chunks} chunks x {cd.chunk_len}, batch {cd.batch}")
+    passes = {}
+
+    def tr(d, chunk, pas, pos, ent, h):
+        if d == 0:
+            passes[chunk] = max(passes.get(chunk, 0), pas + 1)
+
+    with dl.Model(w.model, max_chunk=cd.chunk_len, max_batch=cd.batch) as m:
+        t0 = time.time()
+        data = m.encode(toks, cd)
+        t1 = time.time()
+        back = m.decode(data)
+        t2 = time.time()
+    assert np.array_equal(back, toks)
+    log(f"{name}: {len(toks)} tokens -> {len(data)} bytes "
+        f"({8 * len(data) / (len(toks) * w.token_bytes):.3f} bits/input byte), "
+        f"encode {t1 - t0:.1f}s decode {t2 - t1:.1f}s")
+    return data
+
+
+def test_roundtrip_small_config():
+    roundtrip_workload("small", 4, batch=4)
+
+
+def test_roundtrip_8b_config():
+    roundtrip_workload("8b", 1)
+
+
+def test_roundtrip_8b_threshold_schedule():
+    # tau = 0.5 bits, 1..64 positions per pass; report the pass count
+    w = wl.WORKLOADS["8b-throughput"]
+    cd = dataclasses.replace(w.codec, batch=2)
+    toks = wl.make_tokens(w, 2 * cd.chunk_len)
+    counts = []
+
+    def tr(d, chunk, pas, pos, ent, h):
+        if d == 0:
+            counts.append((chunk, len(pos)))
+
+    with dl.Model(w.model, max_chunk=cd.chunk_len, max_batch=2) as m:
+        m.set_trace(tr)
+        data = m.encode(toks, cd)
+        m.set_trace(None)
+        back = m.decode(data)
+    assert np.array_equal(back, toks)
+    per_chunk = [sum(1 for c, _ in counts if c == k) for k in range(2)]
+    assert all(1 <= n <= 64 for _, n in counts)
+    log("8b-throughput passes per chunk", per_chunk)
+
+
+def test_roundtrip_8b_long_chunk():
+    roundtrip_workload("8b-long", 1, batch=1)
+
+
+def test_logits_8b_full_width_one_layer():
+    sh = wl.with_layers(wl.DLM8B, 1)
+    T = 2048
+    st = wl.random_state(21, 1, T, sh.vocab, 0.5)
+    st[0, 0] = sh.mask_id
+    cols = np.sort(np.random.default_rng(0).choice(sh.vocab, 4096, replace=False))
+    log("8b full width L=1 logits", T)
+    with dl.Model(sh, max_chunk=T, max_batch=1) as m:
+        lg, rows = m.forward_logits(dev_state(st))
+        gpu = lg[:, torch.from_numpy(cols).cuda()].cpu().numpy()
+        rows = rows.cpu().numpy()
+    W = OW.Weights(sh)
+    ref, pos = OM.logits(sh, W, st[0], vocab_rows=cols)
+    assert np.array_equal(rows, pos)
+    err = rel_err_rows(gpu, ref)
+    log("max rel err", err)
+    assert err <= 2e-2
+
+
+def test_logits_long_chunk_attention():
+    # T = 8192 non-causal attention with head dim 128 (one head)
+    sh = shape(d_model=128, n_heads=1, d_ffn=128, n_layers=1, vocab=300, ffn="swiglu",
+               norm="rmsnorm")
+    T = 8192
+    st = wl.random_state(5, 1, T, sh.vocab, 0.3)
+    log("attention T=8192")
+    with dl.Model(sh, max_chunk=T, max_batch=1) as m:
+        lg, rows = m.forward_logits(dev_state(st))
+        lg, rows = lg.cpu().numpy(), rows.cpu().numpy()
+    ref, pos = OM.logits(sh, OW.Weights(sh), st[0])
+    assert np.array_equal(rows, pos)
+    err = rel_err_rows(lg, ref)
+    log("max rel err", err)
+    assert err <= 2e-2

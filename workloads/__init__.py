@@ -90,20 +90,25 @@ def fan_in_exp(fan_in: int) -> int:
     return int(round(0.5 * math.log2(fan_in / 3.0)))
 
 
-def _shape(name, L, d, H, F, V, ffn, norm, dtype, head_exp=None, seed=0):
+def _shape(name, L, d, H, F, V, ffn, norm, dtype, head_exp=None, attn_exp=None, seed=0):
     return ModelShape(
         name=name, n_layers=L, d_model=d, n_heads=H, d_ffn=F, vocab=V, ffn=ffn,
-        norm=norm, dtype=dtype, embed_exp=0, attn_exp=fan_in_exp(d),
+        norm=norm, dtype=dtype, embed_exp=0,
+        attn_exp=fan_in_exp(d) if attn_exp is None else attn_exp,
         ffn_in_exp=fan_in_exp(d), ffn_out_exp=fan_in_exp(F),
         head_exp=fan_in_exp(d) if head_exp is None else head_exp, seed=seed)
 
 
 TINY = _shape("tiny-f32", 2, 128, 4, 512, 256, "gelu", "layernorm", "f32")
 SMALL = _shape("small-bf16", 12, 768, 12, 3072, 32768, "gelu", "layernorm", "bf16")
-# the 8B-shaped model: its head uses 2**-2 so that logit spread (std ~9) gives a
-# realistic mix of confident and uncertain rows at random init.
+# The 8B-shaped model.  Its head uses 2**-2 (logit std ~9) and its attention
+# projections twice the fan-in scale: with fan-in attention a random-init
+# model attends almost uniformly, every masked position gets nearly the same
+# prediction and the 0.5-bit threshold schedule never fires; sharper attention
+# makes predictions position specific, with roughly a fifth of the positions
+# under 0.5 bits, as a trained model would have some confident positions.
 DLM8B = _shape("8b-bf16", 32, 4096, 32, 12288, 126464, "swiglu", "rmsnorm", "bf16",
-               head_exp=2)
+               head_exp=2, attn_exp=fan_in_exp(4096) - 1)
 
 
 @dataclasses.dataclass(frozen=True)
