@@ -94,6 +94,45 @@ def cpu_baseline(w, layers_timed=1, vocab_sample=4096):
     }
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ffn_in_gemm_8b_traffic.md")
+GEMM_SOURCE = os.path.join(ROOT, "paper_2608_11249_amd", "csrc", "gemm_bf16.hip")
+
+
+def gemm_source_hash():
+    import hashlib
+    return hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per launch of the FFN-in GEMM from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE summary, if it was taken on the current source."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    vals = {}
+    for line in open(TRAFFIC_FILE):
+        if ":" in line and line.startswith("- "):
+            k, v = line[2:].split(":", 1)
+            vals[k.strip()] = v.strip().strip("`")
+    if vals.get("gemm_bf16.hip sha256[:16]") != gemm_source_hash():
+        return None
+    try:
+        return float(vals["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def copy_calibration(nbytes):
+    """A plain device-to-device copy of known size, run under rocprofv3 --pmc to
+    scale FETCH_SIZE / WRITE_SIZE into bytes."""
+    import torch
+    x = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(3):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": nbytes, "dispatches": 3}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -102,7 +141,12 @@ def main():
     ap.add_argument("--workload", default="8b",
                     choices=["tiny", "small", "8b", "8b-throughput", "8b-long"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device copy of BYTES (counter calibration)")
     args = ap.parse_args()
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
     if args.gpus != 1:
         print("bench.py runs on one GPU only: the compression path shards by independent "
               "chunks (see DESIGN.md); --gpus must be 1", file=sys.stderr)
@@ -174,7 +218,7 @@ def main():
             "peak": peak,
             "unit": "TFLOP/s",
             "frac": round(achieved / peak, 4),
-            "traffic": None,
+            "traffic": measured_traffic() if (dom == "ffn_in" and args.workload == "8b") else None,
         },
         "detail": {
             "tokens_per_s": coded / elapsed,
