@@ -21,6 +21,23 @@ namespace {
 constexpr int KT = 64;   // keys per tile
 constexpr int QB = 128;  // queries per block (4 waves x 32)
 
+// LDS swizzles for gfx950's 64 four-byte banks (256 B per cycle).
+// K tile: rows of DH bf16; the 16 keys a 16-lane ds_read_b128 group reads in
+// one k step must hit 16 distinct 16-byte slots: with 256-byte rows (DH = 128)
+// XOR the chunk with key & 15, with 128-byte rows (DH = 64) rows r and r + 2
+// share banks, so XOR with (key >> 1) & 7.
+template <int DH>
+__device__ __forceinline__ int kswz(int key) {
+  return DH == 128 ? (key & 15) : ((key >> 1) & 7);
+}
+// V^T tile: rows d of 64 keys (128 B) in 8-byte units; the 32 rows a 32-lane
+// ds_read_b64 group reads must hit 32 distinct 8-byte slots: rows d and d + 2
+// share banks, so unit u of row d is stored at u ^ ((d >> 1) & 15).
+__device__ __forceinline__ int vswz(int d) { return (d >> 1) & 15; }
+
+// 2^x for x <= 0 (or -inf) with the hardware exponential
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
 template <int DH>
 __global__ void __launch_bounds__(256)
 attn_bf16_kernel(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kg,
@@ -66,14 +83,14 @@ attn_bf16_kernel(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kg,
 #pragma unroll
     for (int j = 0; j < K_CH; ++j) {
       const int c = tid + 256 * j, key = c / DC, dc = c % DC;
-      *reinterpret_cast<u32x4*>(&Ks[buf][key * DH + ((dc ^ (key & 7)) << 3)]) = rk[j];
+      *reinterpret_cast<u32x4*>(&Ks[buf][key * DH + ((dc ^ kswz<DH>(key)) << 3)]) = rk[j];
     }
 #pragma unroll
     for (int j = 0; j < V_CH; ++j) {
       // V^T row d holds 16 8-byte units (4 keys each); unit u is stored at
-      // u ^ (d & 15).  A 16-byte chunk = units (2kc, 2kc+1) lands on the unit
+      // u ^ vswz(d).  A 16-byte chunk = units (2kc, 2kc+1) lands on the unit
       // pair kc ^ (x >> 1), halves swapped when x is odd.
-      const int c = tid + 256 * j, d = c >> 3, kc = c & 7, x = d & 15;
+      const int c = tid + 256 * j, d = c >> 3, kc = c & 7, x = vswz(d);
       u32x4 v = rv[j];
       if (x & 1) v = u32x4{v.z, v.w, v.x, v.y};
       *reinterpret_cast<u32x4*>(&Vs[buf][d * KT + ((kc ^ (x >> 1)) << 3)]) = v;
@@ -103,8 +120,8 @@ attn_bf16_kernel(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kg,
     for (int s = 0; s < DH / 16; ++s) {
       const int dc = s * 2 + lg;
       const int key0 = lr, key1 = 32 + lr;
-      const bf16x8 k0f = *reinterpret_cast<const bf16x8*>(&Ks[cur][key0 * DH + ((dc ^ (key0 & 7)) << 3)]);
-      const bf16x8 k1f = *reinterpret_cast<const bf16x8*>(&Ks[cur][key1 * DH + ((dc ^ (key1 & 7)) << 3)]);
+      const bf16x8 k0f = *reinterpret_cast<const bf16x8*>(&Ks[cur][key0 * DH + ((dc ^ kswz<DH>(key0)) << 3)]);
+      const bf16x8 k1f = *reinterpret_cast<const bf16x8*>(&Ks[cur][key1 * DH + ((dc ^ kswz<DH>(key1)) << 3)]);
       s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0f, qf[s], s0, 0, 0, 0);
       s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1f, qf[s], s1, 0, 0, 0);
     }
@@ -121,12 +138,12 @@ attn_bf16_kernel(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kg,
     }
     mx = fmaxf(mx, __shfl_xor(mx, 32));
     const float m_new = fmaxf(m_run, mx);
-    const float alpha = exp2f(m_run - m_new);
+    const float alpha = fast_exp2(m_run - m_new);
     float psum = 0.0f;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      s0[r] = exp2f(s0[r] - m_new);
-      s1[r] = exp2f(s1[r] - m_new);
+      s0[r] = fast_exp2(s0[r] - m_new);
+      s1[r] = fast_exp2(s1[r] - m_new);
       psum += s0[r] + s1[r];
     }
     psum += __shfl_xor(psum, 32);
@@ -150,7 +167,7 @@ attn_bf16_kernel(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kg,
     }
 #pragma unroll
     for (int t = 0; t < DH / 32; ++t) {
-      const int d = t * 32 + lr, x = d & 15;
+      const int d = t * 32 + lr, x = vswz(d);
       const bf16_t* vrow = &Vs[cur][d * KT];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {

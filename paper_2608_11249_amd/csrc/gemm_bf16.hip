@@ -5,14 +5,14 @@
 // grid; each wave owns a (BM/2) x (BN/2) sub-tile built from
 // v_mfma_f32_32x32x16_bf16 tiles.  Operand tiles move global -> LDS with
 // direct loads (global_load_lds_dwordx4) into a double-buffered LDS tile, one
-// barrier per k-tile.  LDS rows are 64 bf16 (128 B); the eight 16-byte chunks
-// of row r are XOR-swizzled by (r & 7) so the ds_read_b128 fragment loads of
-// 8 consecutive rows hit 8 distinct bank groups.  The fragment reads of k step
+// barrier per k-tile.  LDS rows are 64 bf16 (128 B) with the eight 16-byte
+// chunks XOR-swizzled (swz below) so fragment loads are free of bank conflicts.  The fragment reads of k step
 // s + 1 are scheduled between the MFMAs of step s.
 //
 // Measured on MI355X (M = 2048): the fill of LDS from L2 (about 44 B/clk/CU at
-// best, latency-bound per CU) limits these shapes, so 128 x 128 tiles with two
-// blocks per CU win for the forward GEMMs; 256 x 256 wins for the LM head.
+// best, latency-bound per CU) limits these shapes; two waves per SIMD (the
+// 8-wave variant) hide it best for the forward GEMMs, and the 4-wave
+// 256 x 256 tile is best for the LM head.
 //
 // Numerics: each output element is a sequential sum over k-tiles, each k-tile
 // four MFMA steps in order, independent of the tile shape and of which other
@@ -24,6 +24,31 @@ namespace {
 
 constexpr int BK = 64;
 
+// LDS swizzle of the 16-byte chunks of a 128-byte tile row.  gfx950 serves a
+// ds_read_b128 16 lanes at a time from 64 four-byte banks (256 B): rows r and
+// r + 2 start on the same bank, so chunk c of row r is stored at position
+// c ^ ((r >> 1) & 7) -- the 16 rows a 16-lane group reads then cover the 16
+// distinct 16-byte bank slots (8 for even rows, 8 for odd rows).
+__device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
+
+// Tile of block `bid`.  Hardware block ids go round robin over the 8 XCDs;
+// the remap gives each XCD a contiguous range of logical tiles, and the
+// logical order walks groups of 8 m-tiles (m fastest inside a group), so the
+// blocks resident on one XCD at a time cover about 8 x 8 tiles and share their
+// operand panels through that XCD's L2.
+__device__ __forceinline__ void tile_coords(int n_tm, int n_tn, int& tm, int& tn) {
+  int l = blockIdx.x;
+  const int nb = gridDim.x;
+  if ((nb & 7) == 0) l = (l & 7) * (nb >> 3) + (l >> 3);
+  constexpr int G = 8;
+  const int per_group = G * n_tn;
+  const int g = l / per_group, first = g * G;
+  const int gsize = min(n_tm - first, G);
+  const int r = l - g * per_group;
+  tm = first + r % gsize;
+  tn = r / gsize;
+}
+
 __device__ __forceinline__ float gelu_erf(float v) {
   return 0.5f * v * (1.0f + erff(v * 0.70710678118654752440f));
 }
@@ -31,10 +56,9 @@ __device__ __forceinline__ float silu(float v) { return v / (1.0f + expf(-v)); }
 
 // acc[i][j][r] holds C[row][col] with row = i*32 + (r/4)*8 + lg*4 + r%4 and
 // col = j*32 + lr inside the wave tile of wave (wm, wn).
-template <int BM, int BN, int EPI>
-__device__ __forceinline__ void epilogue(f32x16 (&acc)[BM / 64][BN / 64], int m0, int n0, int wm,
-                                         int wn, int lane, int Mv, int N, const EpiArgs& ea) {
-  constexpr int WM = BM / 2, WN = BN / 2;
+template <int BM, int BN, int EPI, int WM, int WN>
+__device__ __forceinline__ void epilogue_w(f32x16 (&acc)[WM / 32][WN / 32], int m0, int n0, int wm,
+                                           int wn, int lane, int Mv, int N, const EpiArgs& ea) {
   constexpr int TM = WM / 32, TN = WN / 32;
   const int lr = lane & 31, lg = lane >> 5;
   const int wrow0 = m0 + wm * WM, wcol0 = n0 + wn * WN;
@@ -106,6 +130,12 @@ __device__ __forceinline__ void epilogue(f32x16 (&acc)[BM / 64][BN / 64], int m0
   }
 }
 
+template <int BM, int BN, int EPI>
+__device__ __forceinline__ void epilogue(f32x16 (&acc)[BM / 64][BN / 64], int m0, int n0, int wm,
+                                         int wn, int lane, int Mv, int N, const EpiArgs& ea) {
+  epilogue_w<BM, BN, EPI, BM / 2, BN / 2>(acc, m0, n0, wm, wn, lane, Mv, N, ea);
+}
+
 // 16-byte direct global -> LDS load (global_load_lds_dwordx4).  `lds` must be
 // wave-uniform: lane l writes lds + 16 l bytes.  The builtin exists only for
 // the device target, so the host pass sees an empty body.
@@ -123,7 +153,7 @@ __device__ __forceinline__ void load_frags(bf16x8 (&f)[NT], const bf16_t* base, 
 #pragma unroll
   for (int i = 0; i < NT; ++i) {
     const int row = w0 + i * 32 + lr;
-    f[i] = *reinterpret_cast<const bf16x8*>(base + row * BK + ((kc ^ (row & 7)) << 3));
+    f[i] = *reinterpret_cast<const bf16x8*>(base + row * BK + ((kc ^ swz(row)) << 3));
   }
 }
 
@@ -139,13 +169,13 @@ __device__ __forceinline__ void mfma_block(f32x16 (&acc)[TM][TN], const bf16x8 (
 
 // Each wave load instruction fills one contiguous 1 KB LDS window (8 tile
 // rows); the XOR swizzle is applied on the global side, lane l of the window
-// fetching chunk (l & 7) ^ (row & 7) of its row.  No VGPR staging, no
+// fetching chunk (l & 7) ^ swz(row) of its row.  No VGPR staging, no
 // ds_write.  MFMA fragments are double buffered in registers across the four
 // k steps.
 template <int BM, int BN, int EPI>
 __global__ void __launch_bounds__(256)
 gemm_bf16_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, int M, int N,
-                 int K, const int* __restrict__ M_dev, EpiArgs ea, int n_tm) {
+                 int K, const int* __restrict__ M_dev, EpiArgs ea, int n_tm, int n_tn) {
   constexpr int WM = BM / 2, WN = BN / 2;
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr int A_IN = BM / 32;  // 1 KB load instructions per wave per k-tile
@@ -156,10 +186,8 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, in
   const int wm = wave >> 1, wn = wave & 1;
   const int lr = lane & 31, lg = lane >> 5;
   const int Mv = M_dev ? min(*M_dev, M) : M;
-  int bid = blockIdx.x;
-  const int nb = gridDim.x;
-  if ((nb & 7) == 0) bid = (bid & 7) * (nb >> 3) + (bid >> 3);
-  const int tm = bid % n_tm, tn = bid / n_tm;
+  int tm, tn;
+  tile_coords(n_tm, n_tn, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
   if (m0 >= Mv) return;
 
@@ -169,12 +197,12 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, in
 #pragma unroll
   for (int j = 0; j < A_IN; ++j) {
     const int sl = (wave * A_IN + j) * 64 + lane, row = sl >> 3;
-    a_off[j] = min(m0 + row, Mv - 1) * K + (((sl & 7) ^ (row & 7)) << 3);
+    a_off[j] = min(m0 + row, Mv - 1) * K + (((sl & 7) ^ swz(row)) << 3);
   }
 #pragma unroll
   for (int j = 0; j < B_IN; ++j) {
     const int sl = (wave * B_IN + j) * 64 + lane, row = sl >> 3;
-    b_off[j] = min(n0 + row, N - 1) * K + (((sl & 7) ^ (row & 7)) << 3);
+    b_off[j] = min(n0 + row, N - 1) * K + (((sl & 7) ^ swz(row)) << 3);
   }
   const int a_win = wave * A_IN * 512, b_win = wave * B_IN * 512;  // this wave's LDS windows
 
@@ -250,12 +278,139 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, in
   epilogue<BM, BN, EPI>(acc, m0, n0, wm, wn, lane, Mv, N, ea);
 }
 
+// 8-wave variant (2 x 4 waves, two per SIMD): wave tile (BM/2) x (BN/4).
+template <int BM, int BN, int EPI>
+__global__ void __launch_bounds__(512)
+gemm_bf16_w8_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, int M, int N,
+                 int K, const int* __restrict__ M_dev, EpiArgs ea, int n_tm, int n_tn) {
+  constexpr int WM = BM / 2, WN = BN / 4;  // 8 waves: 2 x 4
+  constexpr int TM = WM / 32, TN = WN / 32;
+  constexpr int A_IN = BM / 64;  // 1 KB load instructions per wave per k-tile
+  constexpr int B_IN = BN / 64;
+  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * (BM + BN) * BK];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 2, wn = wave & 3;
+  const int lr = lane & 31, lg = lane >> 5;
+  const int Mv = M_dev ? min(*M_dev, M) : M;
+  int tm, tn;
+  tile_coords(n_tm, n_tn, tm, tn);
+  const int m0 = tm * BM, n0 = tn * BN;
+  if (m0 >= Mv) return;
+
+  bf16_t* As = smem;
+  bf16_t* Bs = smem + 2 * BM * BK;
+  int a_off[A_IN], b_off[B_IN];
+#pragma unroll
+  for (int j = 0; j < A_IN; ++j) {
+    const int sl = (wave * A_IN + j) * 64 + lane, row = sl >> 3;
+    a_off[j] = min(m0 + row, Mv - 1) * K + (((sl & 7) ^ swz(row)) << 3);
+  }
+#pragma unroll
+  for (int j = 0; j < B_IN; ++j) {
+    const int sl = (wave * B_IN + j) * 64 + lane, row = sl >> 3;
+    b_off[j] = min(n0 + row, N - 1) * K + (((sl & 7) ^ swz(row)) << 3);
+  }
+  const int a_win = wave * A_IN * 512, b_win = wave * B_IN * 512;  // this wave's LDS windows
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  const int nk = K / BK;
+#pragma unroll
+  for (int j = 0; j < A_IN; ++j)
+    lds_dma16(A + a_off[j], As + a_win + j * 512);
+#pragma unroll
+  for (int j = 0; j < B_IN; ++j)
+    lds_dma16(Bw + b_off[j], Bs + b_win + j * 512);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < nk) {
+      const int k1 = (kt + 1) * BK;
+      bf16_t* an = As + (cur ^ 1) * BM * BK + a_win;
+      bf16_t* bn = Bs + (cur ^ 1) * BN * BK + b_win;
+#pragma unroll
+      for (int j = 0; j < A_IN; ++j)
+        lds_dma16(A + a_off[j] + k1, an + j * 512);
+#pragma unroll
+      for (int j = 0; j < B_IN; ++j)
+        lds_dma16(Bw + b_off[j] + k1, bn + j * 512);
+    }
+    const bf16_t* as = As + cur * BM * BK;
+    const bf16_t* bs = Bs + cur * BN * BK;
+    bf16x8 a0[TM], b0[TN], a1[TM], b1[TN];
+    load_frags<TM>(a0, as, wm * WM, lr, lg);
+    load_frags<TN>(b0, bs, wn * WN, lr, lg);
+    load_frags<TM>(a1, as, wm * WM, lr, 2 + lg);
+    load_frags<TN>(b1, bs, wn * WN, lr, 2 + lg);
+    mfma_block<TM, TN>(acc, a0, b0);
+    load_frags<TM>(a0, as, wm * WM, lr, 4 + lg);
+    load_frags<TN>(b0, bs, wn * WN, lr, 4 + lg);
+    mfma_block<TM, TN>(acc, a1, b1);
+    load_frags<TM>(a1, as, wm * WM, lr, 6 + lg);
+    load_frags<TN>(b1, bs, wn * WN, lr, 6 + lg);
+    mfma_block<TM, TN>(acc, a0, b0);
+    mfma_block<TM, TN>(acc, a1, b1);
+    {
+      // software pipeline: the DS reads of k step s+1 and the direct loads of
+      // the next k-tile are spread between the MFMAs of k step s
+      constexpr int NF = TM + TN, NM = TM * TN, NV = A_IN + B_IN;
+      __builtin_amdgcn_sched_group_barrier(0x100, NF, 0);
+#pragma unroll
+      for (int i = 0; i < NF; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        if (i < NV) __builtin_amdgcn_sched_group_barrier(0x020, NV / NF > 0 ? NV / NF : 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, NM / NF, 0);
+      }
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+        for (int i = 0; i < NF; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, NM / NF, 0);
+        }
+      __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+  }
+  epilogue_w<BM, BN, EPI, WM, WN>(acc, m0, n0, wm, wn, lane, Mv, N, ea);
+}
+
+template <int BM, int BN, int EPI>
+void launch_w8(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int K,
+               const int* M_dev, const EpiArgs& ea) {
+  const int n_tm = ceil_div(M, BM), n_tn = ceil_div(N, BN);
+  gemm_bf16_w8_kernel<BM, BN, EPI><<<dim3(n_tm * n_tn), dim3(512), 0, st>>>(A, B, M, N, K, M_dev, ea, n_tm, n_tn);
+  DLMC_HIP(hipGetLastError());
+}
+
 template <int BM, int BN, int EPI>
 void launch_epi(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int K,
                 const int* M_dev, const EpiArgs& ea) {
   const int n_tm = ceil_div(M, BM), n_tn = ceil_div(N, BN);
-  gemm_bf16_kernel<BM, BN, EPI><<<dim3(n_tm * n_tn), dim3(256), 0, st>>>(A, B, M, N, K, M_dev, ea, n_tm);
+  gemm_bf16_kernel<BM, BN, EPI><<<dim3(n_tm * n_tn), dim3(256), 0, st>>>(A, B, M, N, K, M_dev, ea, n_tm, n_tn);
   DLMC_HIP(hipGetLastError());
+}
+
+template <int BM, int BN>
+void launch_waves8(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int K,
+                   const int* M_dev, EpiKind epi, const EpiArgs& ea) {
+  switch (epi) {
+    case EPI_STORE_F32: launch_w8<BM, BN, EPI_STORE_F32>(st, A, B, M, N, K, M_dev, ea); break;
+    case EPI_RESIDUAL: launch_w8<BM, BN, EPI_RESIDUAL>(st, A, B, M, N, K, M_dev, ea); break;
+    case EPI_GELU: launch_w8<BM, BN, EPI_GELU>(st, A, B, M, N, K, M_dev, ea); break;
+    case EPI_QKV_ROPE: launch_w8<BM, BN, EPI_QKV_ROPE>(st, A, B, M, N, K, M_dev, ea); break;
+    case EPI_SWIGLU: launch_w8<BM, BN, EPI_SWIGLU>(st, A, B, M, N, K, M_dev, ea); break;
+  }
 }
 
 template <int BM, int BN>
@@ -288,13 +443,23 @@ void gemm_bf16(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, i
   if (M <= 0 || N <= 0) return;
   const bool paired = (epi == EPI_QKV_ROPE || epi == EPI_SWIGLU);
   DLMC_CHECK(!paired || N % 128 == 0, DLMC_E_INVAL, "paired epilogue needs N % 128 == 0");
-  // Tile choice (never changes the result): 256 x 256 for the fp32-store
-  // (LM head) when enough rows are live, 128 x 128 otherwise.
+  // Tile choice (never changes the result), from measurements at M = 2048
+  // with the weights streamed from HBM as in a layer loop:
+  //  - LM head (fp32 store): 4-wave 256 x 256 when enough rows are live;
+  //  - at least three 256 x 256 tiles per CU (the SwiGLU FFN-in GEMM): the
+  //    8-wave 256 x 256 kernel;
+  //  - otherwise 4-wave 128 x 128 (two blocks per CU).
   const int live = rows_hint >= 0 ? std::min(rows_hint, M) : M;
-  if (epi == EPI_STORE_F32 && N % 256 == 0 && live >= 512)
-    launch<256, 256>(st, A, B, M, N, K, M_dev, epi, ea);
-  else
+  if (epi == EPI_STORE_F32) {
+    if (N % 256 == 0 && live >= 512)
+      launch<256, 256>(st, A, B, M, N, K, M_dev, epi, ea);
+    else
+      launch<128, 128>(st, A, B, M, N, K, M_dev, epi, ea);
+  } else if (N % 256 == 0 && (long)ceil_div(live, 256) * (N / 256) >= 3 * 256) {
+    launch_waves8<256, 256>(st, A, B, M, N, K, M_dev, epi, ea);
+  } else {
     launch<128, 128>(st, A, B, M, N, K, M_dev, epi, ea);
+  }
 }
 
 }  // namespace dlmc
