@@ -60,7 +60,7 @@ typedef int32_t dlmc_status;
 typedef struct dlmc_model_config {
   uint32_t struct_size; /* sizeof(dlmc_model_config) */
   int32_t n_layers;     /* >= 0 */
-  int32_t d_model;      /* multiple of 64 (bf16) or 16 (f32) */
+  int32_t d_model;      /* multiple of 128 (bf16) or 16 (f32) */
   int32_t n_heads;      /* d_model / n_heads in {64, 128} (bf16), <= 128 (f32) */
   int32_t d_ffn;        /* multiple of 64 (bf16) or 16 (f32) */
   int32_t vocab;        /* |Sigma| >= 2; 2^cdf_bits must exceed it */

@@ -136,6 +136,188 @@ __device__ __forceinline__ void epilogue(f32x16 (&acc)[BM / 64][BN / 64], int m0
   epilogue_w<BM, BN, EPI, BM / 2, BN / 2>(acc, m0, n0, wm, wn, lane, Mv, N, ea);
 }
 
+// ---------------------------------------------------------------------------
+// LDS-staged epilogue.  After the main loop the LDS tile is free: phase 1 has
+// every wave apply its epilogue arithmetic in registers (the same operations,
+// in the same order, as epilogue_w) and park the results in an LDS tile;
+// phase 2 has all threads move 16-byte chunks from LDS to global memory, so
+// stores are coalesced -- including V, which the QKV epilogue writes
+// transposed ([dh, Tp] per head).  Rows of an LDS tile carry 8 elements of
+// padding, which puts the two row groups a wave writes at once on different
+// banks.
+template <int BM, int BN, int EPI>
+struct StagedEpi {
+  static constexpr int PF = BN + 8;       // fp32 tile pitch (STORE, RESIDUAL)
+  static constexpr int PB = BN + 8;       // bf16 tile pitch (GELU, Q/K)
+  static constexpr int PS = BN / 2 + 8;   // bf16 tile pitch (SwiGLU output)
+  static constexpr int PV = BM + 8;       // bf16 dim-major pitch (V)
+  static constexpr int bytes =
+      (EPI == EPI_STORE_F32 || EPI == EPI_RESIDUAL) ? BM * PF * 4
+      : EPI == EPI_GELU                              ? BM * PB * 2
+      : EPI == EPI_SWIGLU                            ? BM * PS * 2
+      : (BM * PB > BN * PV ? BM * PB : BN * PV) * 2;
+  static constexpr int main_bytes = 2 * (BM + BN) * BK * 2;
+  // staged only where it keeps the blocks-per-CU count of the main loop
+  static constexpr int lds_cu = 160 * 1024;
+  static constexpr bool enabled =
+      bytes <= lds_cu && lds_cu / (bytes > main_bytes ? bytes : main_bytes) == lds_cu / main_bytes;
+  static constexpr int smem_elems = (enabled && bytes > main_bytes ? bytes : main_bytes) / 2;
+};
+
+template <int BM, int BN, int EPI, int WM, int WN, int NT>
+__device__ __forceinline__ void epilogue_staged(f32x16 (&acc)[WM / 32][WN / 32], bf16_t* smem,
+                                                int m0, int n0, int wm, int wn, int tid, int Mv,
+                                                int N, const EpiArgs& ea) {
+  using SE = StagedEpi<BM, BN, EPI>;
+  constexpr int TM = WM / 32, TN = WN / 32;
+  const int lane = tid & 63, lr = lane & 31, lg = lane >> 5;
+  const int wr0 = wm * WM, wc0 = wn * WN;  // wave tile origin inside the block tile
+  float* sf = reinterpret_cast<float*>(smem);
+  // the main loop's last barrier ends every read of the operand tiles
+  if constexpr (EPI == EPI_STORE_F32 || EPI == EPI_RESIDUAL || EPI == EPI_GELU) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = wr0 + i * 32 + (r >> 2) * 8 + lg * 4 + (r & 3), col = wc0 + j * 32 + lr;
+          if constexpr (EPI == EPI_GELU)
+            smem[row * SE::PB + col] = f32_to_bf16(gelu_erf(acc[i][j][r]));
+          else
+            sf[row * SE::PF + col] = acc[i][j][r];
+        }
+  } else if constexpr (EPI == EPI_SWIGLU) {
+#pragma unroll
+    for (int j = 0; j < TN; j += 2)
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = wr0 + i * 32 + (r >> 2) * 8 + lg * 4 + (r & 3);
+          const int f = (wc0 + j * 32) / 2 + lr;
+          smem[row * SE::PS + f] = f32_to_bf16(silu(acc[i][j][r]) * acc[i][j + 1][r]);
+        }
+  } else {  // EPI_QKV_ROPE: the block tile lies inside one of Q, K, V (d % BN == 0)
+    const int d = ea.d, dh = ea.dh, T = ea.T, half = dh / 2;
+    const int which = n0 / d;
+    if (which < 2) {
+#pragma unroll
+      for (int j = 0; j < TN; j += 2) {
+        const int lc0 = wc0 + j * 32;               // local column of the (lo, hi) pair
+        const int in_head = (n0 + lc0) % d % dh;
+        const int hb = lc0 - in_head;               // local column of the head's first dim
+        const int dlo = ((in_head / 32) >> 1) * 32 + lr;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int row = wr0 + i * 32 + (r >> 2) * 8 + lg * 4 + (r & 3);
+            const int grow = min(m0 + row, Mv - 1);
+            const int t = grow % T;
+            const float lo = acc[i][j][r], hi = acc[i][j + 1][r];
+            const float c = ea.rope_cos[t * half + dlo], s = ea.rope_sin[t * half + dlo];
+            smem[row * SE::PB + hb + dlo] = f32_to_bf16(lo * c - hi * s);
+            smem[row * SE::PB + hb + dlo + half] = f32_to_bf16(hi * c + lo * s);
+          }
+      }
+    } else {
+      // V, dim-major: 4 consecutive rows of one column are one 8-byte write
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int row = wr0 + i * 32 + q * 8 + lg * 4, col = wc0 + j * 32 + lr;
+            u32x2 v;
+            v[0] = (uint32_t)f32_to_bf16(acc[i][j][4 * q]) | ((uint32_t)f32_to_bf16(acc[i][j][4 * q + 1]) << 16);
+            v[1] = (uint32_t)f32_to_bf16(acc[i][j][4 * q + 2]) | ((uint32_t)f32_to_bf16(acc[i][j][4 * q + 3]) << 16);
+            *reinterpret_cast<u32x2*>(smem + col * SE::PV + row) = v;
+          }
+    }
+  }
+  __syncthreads();
+  // phase 2: 16-byte chunks
+  if constexpr (EPI == EPI_STORE_F32 || EPI == EPI_RESIDUAL) {
+    constexpr int CPR = BN / 4;  // float4 chunks per row
+    for (int qi = tid; qi < BM * CPR; qi += NT) {
+      const int row = qi / CPR, c = (qi % CPR) * 4;
+      const int grow = m0 + row, gcol = n0 + c;
+      if (grow >= Mv) continue;
+      float* dst = (float*)ea.out + (size_t)grow * ea.ldo + gcol;
+      const float* src = sf + row * SE::PF + c;
+      if (gcol + 4 <= N && (ea.ldo & 3) == 0) {
+        float4 v = *reinterpret_cast<const float4*>(src);
+        if constexpr (EPI == EPI_RESIDUAL) {
+          const float4 o = *reinterpret_cast<const float4*>(dst);
+          v.x = o.x + v.x; v.y = o.y + v.y; v.z = o.z + v.z; v.w = o.w + v.w;
+        }
+        *reinterpret_cast<float4*>(dst) = v;
+      } else {
+        for (int e = 0; e < 4 && gcol + e < N; ++e) {
+          if constexpr (EPI == EPI_RESIDUAL) dst[e] += src[e];
+          else dst[e] = src[e];
+        }
+      }
+    }
+  } else if constexpr (EPI == EPI_GELU || EPI == EPI_SWIGLU) {
+    constexpr int W = EPI == EPI_GELU ? BN : BN / 2;
+    constexpr int P = EPI == EPI_GELU ? SE::PB : SE::PS;
+    constexpr int CPR = W / 8;
+    const int gc0 = EPI == EPI_GELU ? n0 : n0 / 2;
+    const int Nout = EPI == EPI_GELU ? N : N / 2;
+    for (int qi = tid; qi < BM * CPR; qi += NT) {
+      const int row = qi / CPR, c = (qi % CPR) * 8;
+      const int grow = m0 + row, gcol = gc0 + c;
+      if (grow >= Mv) continue;
+      bf16_t* dst = (bf16_t*)ea.out + (size_t)grow * ea.ldo + gcol;
+      const bf16_t* src = smem + row * P + c;
+      if (gcol + 8 <= Nout && (ea.ldo & 7) == 0) {
+        *reinterpret_cast<u32x4*>(dst) = *reinterpret_cast<const u32x4*>(src);
+      } else {
+        for (int e = 0; e < 8 && gcol + e < Nout; ++e) dst[e] = src[e];
+      }
+    }
+  } else {
+    const int d = ea.d, dh = ea.dh, T = ea.T, Tp = ea.Tp, H = ea.H;
+    const int which = n0 / d, nb = n0 - which * d;  // first column inside Q, K or V
+    if (which < 2) {
+      constexpr int CPR = BN / 8;
+      bf16_t* base = (bf16_t*)(which == 0 ? ea.q : ea.k);
+      for (int qi = tid; qi < BM * CPR; qi += NT) {
+        const int row = qi / CPR, c = (qi % CPR) * 8;
+        const int grow = m0 + row;
+        if (grow >= Mv) continue;
+        const int b = grow / T, t = grow - b * T;
+        const int h = (nb + c) / dh, dim = (nb + c) % dh;
+        bf16_t* dst = base + (((size_t)b * H + h) * Tp + t) * dh + dim;
+        *reinterpret_cast<u32x4*>(dst) = *reinterpret_cast<const u32x4*>(smem + row * SE::PB + c);
+      }
+    } else {
+      constexpr int CPC = BM / 8;  // chunks of 8 rows per column
+      bf16_t* base = (bf16_t*)ea.vt;
+      for (int qi = tid; qi < BN * CPC; qi += NT) {
+        const int col = qi / CPC, r0 = (qi % CPC) * 8;
+        const int grow = m0 + r0;
+        if (grow >= Mv) continue;
+        const int h = (nb + col) / dh, dim = (nb + col) % dh;
+        const int b = grow / T, t = grow - b * T;
+        const bf16_t* src = smem + col * SE::PV + r0;
+        if (t % 8 == 0 && t + 8 <= T && grow + 8 <= Mv) {
+          bf16_t* dst = base + (((size_t)b * H + h) * dh + dim) * Tp + t;
+          *reinterpret_cast<u32x4*>(dst) = *reinterpret_cast<const u32x4*>(src);
+        } else {
+          for (int e = 0; e < 8 && grow + e < Mv; ++e) {
+            const int ge = grow + e, be = ge / T, te = ge - be * T;
+            base[(((size_t)be * H + h) * dh + dim) * Tp + te] = src[e];
+          }
+        }
+      }
+    }
+  }
+}
+
 // 16-byte direct global -> LDS load (global_load_lds_dwordx4).  `lds` must be
 // wave-uniform: lane l writes lds + 16 l bytes.  The builtin exists only for
 // the device target, so the host pass sees an empty body.
@@ -180,7 +362,7 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, in
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr int A_IN = BM / 32;  // 1 KB load instructions per wave per k-tile
   constexpr int B_IN = BN / 32;
-  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * (BM + BN) * BK];
+  __shared__ __attribute__((aligned(16))) bf16_t smem[StagedEpi<BM, BN, EPI>::smem_elems];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
@@ -275,7 +457,10 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, in
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
   }
-  epilogue<BM, BN, EPI>(acc, m0, n0, wm, wn, lane, Mv, N, ea);
+  if constexpr (StagedEpi<BM, BN, EPI>::enabled)
+    epilogue_staged<BM, BN, EPI, BM / 2, BN / 2, 256>(acc, smem, m0, n0, wm, wn, tid, Mv, N, ea);
+  else
+    epilogue<BM, BN, EPI>(acc, m0, n0, wm, wn, lane, Mv, N, ea);
 }
 
 // 8-wave variant (2 x 4 waves, two per SIMD): wave tile (BM/2) x (BN/4).
@@ -287,7 +472,7 @@ gemm_bf16_w8_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw,
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr int A_IN = BM / 64;  // 1 KB load instructions per wave per k-tile
   constexpr int B_IN = BN / 64;
-  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * (BM + BN) * BK];
+  __shared__ __attribute__((aligned(16))) bf16_t smem[StagedEpi<BM, BN, EPI>::smem_elems];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 2, wn = wave & 3;
@@ -382,7 +567,10 @@ gemm_bf16_w8_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw,
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
   }
-  epilogue_w<BM, BN, EPI, WM, WN>(acc, m0, n0, wm, wn, lane, Mv, N, ea);
+  if constexpr (StagedEpi<BM, BN, EPI>::enabled)
+    epilogue_staged<BM, BN, EPI, WM, WN, 512>(acc, smem, m0, n0, wm, wn, tid, Mv, N, ea);
+  else
+    epilogue_w<BM, BN, EPI, WM, WN>(acc, m0, n0, wm, wn, lane, Mv, N, ea);
 }
 
 template <int BM, int BN, int EPI>
@@ -443,6 +631,8 @@ void gemm_bf16(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, i
   if (M <= 0 || N <= 0) return;
   const bool paired = (epi == EPI_QKV_ROPE || epi == EPI_SWIGLU);
   DLMC_CHECK(!paired || N % 128 == 0, DLMC_E_INVAL, "paired epilogue needs N % 128 == 0");
+  DLMC_CHECK(epi != EPI_QKV_ROPE || (ea.d % 128 == 0 && (ea.dh == 64 || ea.dh == 128)),
+             DLMC_E_INVAL, "QKV epilogue needs d % 128 == 0 and head dim 64 or 128");
   // Tile choice (never changes the result), from measurements at M = 2048
   // with the weights streamed from HBM as in a layer loop:
   //  - LM head (fp32 store): 4-wave 256 x 256 when enough rows are live;

@@ -148,8 +148,8 @@ static void validate(const dlmc_model_config& c) {
   DLMC_CHECK(c.d_model <= 8192, DLMC_E_INVAL, "d_model above 8192");
   const int dh = c.d_model / c.n_heads;
   if (c.dtype == DLMC_DTYPE_BF16) {
-    DLMC_CHECK(c.d_model % 64 == 0 && c.d_ffn % 64 == 0, DLMC_E_INVAL,
-               "bf16 model needs d_model and d_ffn multiples of 64");
+    DLMC_CHECK(c.d_model % 128 == 0 && c.d_ffn % 64 == 0, DLMC_E_INVAL,
+               "bf16 model needs d_model a multiple of 128 and d_ffn a multiple of 64");
     DLMC_CHECK(dh == 64 || dh == 128, DLMC_E_INVAL, "bf16 model needs head dim 64 or 128");
   } else {
     DLMC_CHECK(c.d_model % 16 == 0 && c.d_ffn % 16 == 0, DLMC_E_INVAL,
