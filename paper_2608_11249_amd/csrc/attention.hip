@@ -4,15 +4,19 @@
 // included as keys (the bidirectional-conditioning remark after Definition 3):
 // O = softmax(Q K^T / sqrt(dh)) V over all T keys, one chunk per batch entry.
 //
-// bf16 path (gfx950 MFMA): flash-style single pass over 64-key tiles staged
-// in LDS, fp32 online-softmax statistics.  Each wave owns 32 queries and
-// computes S^T = K Q^T with v_mfma_f32_32x32x16_bf16, so one lane holds 32
-// scores of ONE query: the row max / row sum need one cross-lane exchange
-// (lane ^ 32) instead of a 32-lane reduction.  The probabilities then feed
-// O^T += V^T P^T directly from the S^T accumulator registers; the MFMA k-slot
-// order of P^T is a permutation of the keys, and the V^T fragment is read
-// from LDS with the same permutation.  Key tiles are visited in a fixed order,
-// so results do not depend on the launch shape or on other chunks.
+// bf16 path (gfx950 MFMA): flash-style single pass over 64-key tiles with
+// fp32 online-softmax statistics.  Each wave owns 32 queries and computes
+// S^T = K Q^T with v_mfma_f32_32x32x16_bf16, so one lane holds 32 scores of
+// ONE query and the row max / row sum need one cross-lane exchange
+// (lane ^ 32).  The probabilities feed O^T += V^T P^T straight from the S^T
+// accumulator registers.  To make the k-slots of P^T consecutive keys, the K
+// tile is stored in LDS with its rows permuted inside every group of 16
+// (row i holds key sigma(i), bits 2 and 3 of i swapped); the V^T fragment of
+// a lane is then 8 consecutive keys, one ds_read_b128.  Tiles move global ->
+// LDS with direct loads (global_load_lds_dwordx4) into a double buffer, so no
+// registers stage them and two waves fit per SIMD.  Key tiles are visited in
+// a fixed order, so results do not depend on the launch shape or on other
+// chunks.
 #include "kernels.h"
 
 namespace dlmc {
@@ -21,31 +25,42 @@ namespace {
 constexpr int KT = 64;   // keys per tile
 constexpr int QB = 128;  // queries per block (4 waves x 32)
 
-// LDS swizzles for gfx950's 64 four-byte banks (256 B per cycle).
-// K tile: rows of DH bf16; the 16 keys a 16-lane ds_read_b128 group reads in
-// one k step must hit 16 distinct 16-byte slots: with 256-byte rows (DH = 128)
-// XOR the chunk with key & 15, with 128-byte rows (DH = 64) rows r and r + 2
-// share banks, so XOR with (key >> 1) & 7.
+// LDS row i of a K tile holds key sigma(i) of the tile (an involution)
+__device__ __forceinline__ int sigma(int i) { return (i & ~12) | ((i & 4) << 1) | ((i & 8) >> 1); }
+
+// LDS swizzles for gfx950's 64 four-byte banks (256 B per cycle): the 16
+// rows a 16-lane ds_read_b128 group reads must hit 16 distinct 16-byte slots.
+// K rows of DH bf16: with 256-byte rows (DH = 128) XOR the chunk with i & 15;
+// with 128-byte rows (DH = 64) rows i and i + 2 share banks, so XOR with
+// (i >> 1) & 7.  V^T rows are 64 keys (128 bytes): XOR with (d >> 1) & 7.
 template <int DH>
-__device__ __forceinline__ int kswz(int key) {
-  return DH == 128 ? (key & 15) : ((key >> 1) & 7);
+__device__ __forceinline__ int kswz(int i) {
+  return DH == 128 ? (i & 15) : ((i >> 1) & 7);
 }
-// V^T tile: rows d of 64 keys (128 B) in 8-byte units; the 32 rows a 32-lane
-// ds_read_b64 group reads must hit 32 distinct 8-byte slots: rows d and d + 2
-// share banks, so unit u of row d is stored at u ^ ((d >> 1) & 15).
-__device__ __forceinline__ int vswz(int d) { return (d >> 1) & 15; }
+__device__ __forceinline__ int vswz(int d) { return (d >> 1) & 7; }
 
 // 2^x for x <= 0 (or -inf) with the hardware exponential
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// 16-byte direct global -> LDS load; `lds` is wave-uniform, lane l writes
+// lds + 16 l bytes.  The builtin exists only for the device target.
+__device__ __forceinline__ void lds_dma16(const bf16_t* g, bf16_t* lds) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_global_load_lds(g, lds, 16, 0, 0);
+#endif
+}
+
 template <int DH>
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(256, 2)
 attn_bf16_kernel(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kg,
                  const bf16_t* __restrict__ Vt, bf16_t* __restrict__ O, int H, int T, int Tp,
                  float scale_log2) {
-  constexpr int DC = DH / 8;                 // 16-byte chunks per key row
-  constexpr int K_CH = KT * DC / 256;        // K-tile chunks per thread
-  constexpr int V_CH = DH * (KT / 8) / 256;  // V^T-tile chunks per thread
+  constexpr int NS = DH / 16;        // k steps of S^T
+  constexpr int RB = DH * 2;         // bytes per K row
+  constexpr int KRW = 1024 / RB;     // K rows per 1 KB load window
+  constexpr int KW = KT / KRW / 4;   // K windows per wave
+  constexpr int VW = DH / 8 / 4;     // V^T windows (8 rows of 128 B) per wave
+  constexpr int NV = DH / 32 * 4;    // PV MFMAs per tile
   __shared__ __attribute__((aligned(16))) bf16_t Ks[2][KT * DH];
   __shared__ __attribute__((aligned(16))) bf16_t Vs[2][DH * KT];
 
@@ -59,42 +74,33 @@ attn_bf16_kernel(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kg,
   const int q0 = blockIdx.x * QB + wave * 32;
 
   // B operand of S^T = K Q^T: lane holds Q[q0 + lr][16 s + 8 lg .. + 7]
-  bf16x8 qf[DH / 16];
+  bf16x8 qf[NS];
 #pragma unroll
-  for (int s = 0; s < DH / 16; ++s)
+  for (int s = 0; s < NS; ++s)
     qf[s] = *reinterpret_cast<const bf16x8*>(Qp + (size_t)(q0 + lr) * DH + s * 16 + lg * 8);
 
-  // tile loaders (Tp is a multiple of QB, so every row read is inside the buffer;
-  // rows at or beyond T hold finite values and get zero probability)
-  u32x4 rk[K_CH], rv[V_CH];
-  auto gload = [&](int k0) {
+  // Per-lane sources of the direct loads (element offsets inside a tile).  Lane
+  // l of a window fills LDS row i, 16-byte slot p, with chunk p ^ swizzle of
+  // key sigma(i).  Tp is a multiple of 128, so every row read is inside the
+  // buffer; rows at or beyond T hold finite values and get zero probability.
+  int k_src[KW], v_src[VW];
 #pragma unroll
-    for (int j = 0; j < K_CH; ++j) {
-      const int c = tid + 256 * j, key = c / DC, dc = c % DC;
-      rk[j] = *reinterpret_cast<const u32x4*>(Kp + (size_t)(k0 + key) * DH + dc * 8);
-    }
+  for (int w = 0; w < KW; ++w) {
+    const int i = (wave * KW + w) * KRW + lane / (RB / 16), p = lane % (RB / 16);
+    k_src[w] = sigma(i) * DH + ((p ^ kswz<DH>(i)) << 3);
+  }
 #pragma unroll
-    for (int j = 0; j < V_CH; ++j) {
-      const int c = tid + 256 * j, d = c >> 3, kc = c & 7;
-      rv[j] = *reinterpret_cast<const u32x4*>(Vp + (size_t)d * Tp + k0 + kc * 8);
-    }
-  };
-  auto sstore = [&](int buf) {
+  for (int w = 0; w < VW; ++w) {
+    const int d = (wave * VW + w) * 8 + (lane >> 3), p = lane & 7;
+    v_src[w] = d * Tp + ((p ^ vswz(d)) << 3);
+  }
+  auto load_tile = [&](int kt, int buf) {
 #pragma unroll
-    for (int j = 0; j < K_CH; ++j) {
-      const int c = tid + 256 * j, key = c / DC, dc = c % DC;
-      *reinterpret_cast<u32x4*>(&Ks[buf][key * DH + ((dc ^ kswz<DH>(key)) << 3)]) = rk[j];
-    }
+    for (int w = 0; w < KW; ++w)
+      lds_dma16(Kp + (size_t)kt * KT * DH + k_src[w], &Ks[buf][(wave * KW + w) * 512]);
 #pragma unroll
-    for (int j = 0; j < V_CH; ++j) {
-      // V^T row d holds 16 8-byte units (4 keys each); unit u is stored at
-      // u ^ vswz(d).  A 16-byte chunk = units (2kc, 2kc+1) lands on the unit
-      // pair kc ^ (x >> 1), halves swapped when x is odd.
-      const int c = tid + 256 * j, d = c >> 3, kc = c & 7, x = vswz(d);
-      u32x4 v = rv[j];
-      if (x & 1) v = u32x4{v.z, v.w, v.x, v.y};
-      *reinterpret_cast<u32x4*>(&Vs[buf][d * KT + ((kc ^ (x >> 1)) << 3)]) = v;
-    }
+    for (int w = 0; w < VW; ++w)
+      lds_dma16(Vp + kt * KT + v_src[w], &Vs[buf][(wave * VW + w) * 512]);
   };
 
   f32x16 o[DH / 32];
@@ -105,58 +111,67 @@ attn_bf16_kernel(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kg,
   float m_run = -INFINITY, l_run = 0.0f;
 
   const int n_kt = (T + KT - 1) / KT;
-  gload(0);
-  sstore(0);
+  load_tile(0, 0);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   for (int kt = 0; kt < n_kt; ++kt) {
     const int cur = kt & 1, k0 = kt * KT;
-    if (kt + 1 < n_kt) gload(k0 + KT);
+    if (kt + 1 < n_kt) load_tile(kt + 1, cur ^ 1);
 
-    // S^T tiles: keys 0-31 (s0) and 32-63 (s1) of this tile x 32 queries
+    // S^T for LDS rows 0-31 (s0) and 32-63 (s1); fragments two k steps ahead
     f32x16 s0, s1;
 #pragma unroll
     for (int r = 0; r < 16; ++r) s0[r] = s1[r] = 0.0f;
+    const bf16_t* kb = Ks[cur];
+    bf16x8 kf[3][2];
+    auto kload = [&](int s, bf16x8(&f)[2]) {
+      const int dc = 2 * s + lg;
+      f[0] = *reinterpret_cast<const bf16x8*>(kb + lr * DH + ((dc ^ kswz<DH>(lr)) << 3));
+      f[1] = *reinterpret_cast<const bf16x8*>(kb + (32 + lr) * DH + ((dc ^ kswz<DH>(32 + lr)) << 3));
+    };
+    kload(0, kf[0]);
+    kload(1, kf[1]);
 #pragma unroll
-    for (int s = 0; s < DH / 16; ++s) {
-      const int dc = s * 2 + lg;
-      const int key0 = lr, key1 = 32 + lr;
-      const bf16x8 k0f = *reinterpret_cast<const bf16x8*>(&Ks[cur][key0 * DH + ((dc ^ kswz<DH>(key0)) << 3)]);
-      const bf16x8 k1f = *reinterpret_cast<const bf16x8*>(&Ks[cur][key1 * DH + ((dc ^ kswz<DH>(key1)) << 3)]);
-      s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0f, qf[s], s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1f, qf[s], s1, 0, 0, 0);
+    for (int s = 0; s < NS; ++s) {
+      if (s + 2 < NS) kload(s + 2, kf[(s + 2) % 3]);
+      s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s % 3][0], qf[s], s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s % 3][1], qf[s], s1, 0, 0, 0);
     }
 
-    // online softmax (base 2) for query q0 + lr; this lane holds keys
-    // (r/4)*8 + lg*4 + r%4 (+32 for s1) of the tile
+    // online softmax (base 2) for query q0 + lr.  Register r of s0 holds key
+    // 16 (r >> 3) + 8 lg + (r & 7) of the tile (s1: + 32).
+    if (k0 + KT > T) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = k0 + 16 * (r >> 3) + 8 * lg + (r & 7);
+        if (key >= T) s0[r] = -INFINITY;
+        if (key + 32 >= T) s1[r] = -INFINITY;
+      }
+    }
     float mx = -INFINITY;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int key = k0 + (r >> 2) * 8 + lg * 4 + (r & 3);
-      s0[r] = key < T ? s0[r] * scale_log2 : -INFINITY;
-      s1[r] = key + 32 < T ? s1[r] * scale_log2 : -INFINITY;
-      mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
-    }
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
+    mx = fmaxf(mx, __shfl_xor(mx, 32)) * scale_log2;
     const float m_new = fmaxf(m_run, mx);
     const float alpha = fast_exp2(m_run - m_new);
-    float psum = 0.0f;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      s0[r] = fast_exp2(s0[r] - m_new);
-      s1[r] = fast_exp2(s1[r] - m_new);
-      psum += s0[r] + s1[r];
-    }
-    psum += __shfl_xor(psum, 32);
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
+    l_run *= alpha;
 #pragma unroll
     for (int t = 0; t < DH / 32; ++t)
 #pragma unroll
       for (int r = 0; r < 16; ++r) o[t][r] *= alpha;
+    m_run = m_new;
+    float psum = 0.0f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      s0[r] = fast_exp2(fmaf(s0[r], scale_log2, -m_new));
+      s1[r] = fast_exp2(fmaf(s1[r], scale_log2, -m_new));
+      psum += s0[r] + s1[r];
+    }
+    psum += __shfl_xor(psum, 32);
+    l_run += psum;
 
-    // P^T fragments: k-step j covers keys 16j..16j+15 of the tile; this lane's
-    // k-slots 8lg+0..3 are keys 16j+4lg+0..3, slots 8lg+4..7 keys 16j+8+4lg+0..3,
-    // i.e. accumulator registers 8(j%2) .. 8(j%2)+7 of tile j/2.
+    // P^T fragment of k step j: keys 16 j + 8 lg .. + 7 = registers
+    // 8 (j % 2) .. + 7 of tile j / 2
     bf16x8 pf[4];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
@@ -165,20 +180,22 @@ attn_bf16_kernel(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kg,
       pf[2][e] = (__bf16)s1[e];
       pf[3][e] = (__bf16)s1[8 + e];
     }
+    // O^T += V^T P^T; the V^T fragment of row d, k step j is chunk 2 j + lg
+    const bf16_t* vb = Vs[cur];
+    bf16x8 vf[3];
+    auto vload = [&](int idx, bf16x8& f) {
+      const int t = idx >> 2, j = idx & 3, d = t * 32 + lr, c = 2 * j + lg;
+      f = *reinterpret_cast<const bf16x8*>(vb + d * KT + ((c ^ vswz(d)) << 3));
+    };
+    vload(0, vf[0]);
+    vload(1, vf[1]);
 #pragma unroll
-    for (int t = 0; t < DH / 32; ++t) {
-      const int d = t * 32 + lr, x = vswz(d);
-      const bf16_t* vrow = &Vs[cur][d * KT];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int u1 = 4 * j + lg, u2 = 4 * j + 2 + lg;
-        const u32x2 a = *reinterpret_cast<const u32x2*>(vrow + ((u1 ^ x) << 2));
-        const u32x2 c = *reinterpret_cast<const u32x2*>(vrow + ((u2 ^ x) << 2));
-        const bf16x8 vf = __builtin_bit_cast(bf16x8, u32x4{a.x, a.y, c.x, c.y});
-        o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[j], o[t], 0, 0, 0);
-      }
+    for (int idx = 0; idx < NV; ++idx) {
+      if (idx + 2 < NV) vload(idx + 2, vf[(idx + 2) % 3]);
+      o[idx >> 2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[idx % 3], pf[idx & 3], o[idx >> 2], 0, 0, 0);
     }
-    if (kt + 1 < n_kt) sstore(cur ^ 1);
+    // the next tile has landed (own loads) and every wave is done with this one
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
   }
 
