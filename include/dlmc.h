@@ -180,12 +180,14 @@ dlmc_status dlmc_select(dlmc_model* model, const float* entropy_bits, const int3
  * its canonical [out, in] layout: bf16 bit patterns (uint16) or fp32. */
 dlmc_status dlmc_weight_copy(dlmc_model* model, int32_t tensor_id, void* dst, uint64_t bytes);
 
-/* Stage timing for benchmarks: while enabled, every launch of a stage is
+/* Stage timing for benchmarks: every launch of a stage whose bit is set in
+ * `stage_mask` (bit s = DLMC_STAGE_s; DLMC_PROFILE_ALL for all, 0 to stop) is
  * bracketed by HIP events on the model's stream, and the stage's algorithmic
  * work per launch (flops for GEMMs and attention, HBM bytes for the memory
- * bound stages) is accumulated.  Enabling (on = 1) or disabling resets the
- * counters.  dlmc_profile_read synchronises the stream and returns, for
- * `stage` (DLMC_STAGE_*), the summed event time in ms, the number of
+ * bound stages) is accumulated.  Each call resets the counters.  Events cost
+ * a little time per launch, so a throughput measurement should time only the
+ * stages it reports.  dlmc_profile_read synchronises the stream and returns,
+ * for `stage` (DLMC_STAGE_*), the summed event time in ms, the number of
  * launches and the summed work. */
 #define DLMC_STAGE_EMBED 0
 #define DLMC_STAGE_NORM 1
@@ -201,7 +203,8 @@ dlmc_status dlmc_weight_copy(dlmc_model* model, int32_t tensor_id, void* dst, ui
 #define DLMC_STAGE_REVEAL 11
 #define DLMC_STAGE_COMPACT 12
 #define DLMC_N_STAGES 13
-dlmc_status dlmc_profile_enable(dlmc_model* model, int32_t on);
+#define DLMC_PROFILE_ALL ((1u << DLMC_N_STAGES) - 1u)
+dlmc_status dlmc_profile_enable(dlmc_model* model, uint32_t stage_mask);
 dlmc_status dlmc_profile_read(dlmc_model* model, int32_t stage, double* ms_total,
                               uint64_t* launches, double* work);
 

@@ -12,7 +12,7 @@ from __future__ import annotations
 import ctypes
 import os
 import re
-from typing import Callable, Optional
+from typing import Callable, Optional, Sequence
 
 import numpy as np
 
@@ -82,7 +82,7 @@ _SIGS = {
     "dlmc_entropy_cdf": (i32, [vp, vp, i32, i32, vp, vp, vp, vp]),
     "dlmc_select": (i32, [vp, vp, vp, i32, i32, i32, f32, i32, i32, vp, vp, vp]),
     "dlmc_weight_copy": (i32, [vp, i32, vp, u64]),
-    "dlmc_profile_enable": (i32, [vp, i32]),
+    "dlmc_profile_enable": (i32, [vp, ctypes.c_uint32]),
     "dlmc_profile_read": (i32, [vp, i32, P(ctypes.c_double), P(u64), P(ctypes.c_double)]),
     "dlmc_rc_encode": (i32, [vp, vp, u64, i32, i32, vp, u64, P(u64)]),
     "dlmc_rc_decode": (i32, [vp, u64, vp, u64, i32, i32, i32, vp]),
@@ -250,9 +250,18 @@ class Model:
         self._trace_cb = TRACE_FN(cb)
         _check(lib().dlmc_set_trace(self.handle, self._trace_cb, None))
 
-    def profile(self, on: bool):
-        """Enable / disable (and reset) per-stage event timing."""
-        _check(lib().dlmc_profile_enable(self.handle, 1 if on else 0))
+    def profile(self, on: bool = True, stages: Optional[Sequence[str]] = None):
+        """Enable (all stages, or the named ones) / disable per-stage event
+        timing; every call resets the counters."""
+        if not on:
+            mask = 0
+        elif stages is None:
+            mask = (1 << len(STAGES)) - 1
+        else:
+            mask = 0
+            for name in stages:
+                mask |= 1 << STAGES.index(name)
+        _check(lib().dlmc_profile_enable(self.handle, mask))
 
     def profile_read(self) -> dict:
         """{stage: (ms_total, launches, work)} since profiling was enabled."""

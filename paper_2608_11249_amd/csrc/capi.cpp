@@ -292,11 +292,11 @@ dlmc_status dlmc_weight_copy(dlmc_model* m, int32_t tensor_id, void* dst, uint64
   });
 }
 
-dlmc_status dlmc_profile_enable(dlmc_model* m, int32_t on) {
+dlmc_status dlmc_profile_enable(dlmc_model* m, uint32_t stage_mask) {
   return guard([&] {
     use(m);
     m->prof_reset();
-    m->prof = on != 0;
+    m->prof = stage_mask & DLMC_PROFILE_ALL;
   });
 }
 

@@ -60,7 +60,7 @@ struct dlmc_model {
     hipEvent_t a, b;
     double work;
   };
-  bool prof = false;
+  uint32_t prof = 0;  // bit s set: stage s is timed
   std::vector<ProfRec> prof_recs;
   std::vector<hipEvent_t> prof_pool;
   double prof_ms[DLMC_N_STAGES] = {}, prof_work[DLMC_N_STAGES] = {};
@@ -89,7 +89,7 @@ struct StageTimer {
   double work;
   hipEvent_t a = nullptr;
   StageTimer(dlmc_model* m_, int stage_, double work_) : m(m_), stage(stage_), work(work_) {
-    if (m->prof) {
+    if (m->prof & (1u << stage_)) {
       a = m->prof_event();
       DLMC_HIP(hipEventRecord(a, m->stream));
     }

@@ -156,7 +156,7 @@ int dlmc_session::step(uint64_t* coded) {
   if (encode) DLMC_HIP(hipMemcpyAsync(h_sym, m->sym, (size_t)B * mm * 8, hipMemcpyDeviceToHost, s));
   DLMC_HIP(hipStreamSynchronize(s));
   if (*h_err) throw Error(DLMC_E_NUMERIC, "non-finite entropy (non-finite logits)");
-  if (m->prof && cdf_rec < m->prof_recs.size()) {
+  if (cdf_rec < m->prof_recs.size() && m->prof_recs[cdf_rec].stage == DLMC_STAGE_CDF) {
     int64_t committed = 0;
     for (int b = 0; b < B; ++b) committed += h_nsel[b];
     m->prof_recs[cdf_rec].work = (double)committed * (8.0 * V + 4.0);

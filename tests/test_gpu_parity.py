@@ -240,3 +240,28 @@ def test_errors_on_gpu_model():
         with pytest.raises(dl.DlmcError) as e:
             m2.decode(data)
         assert e.value.code == -4
+
+
+def test_stage_profile_mask():
+    """Only the stages named in the profile mask are timed; the CDF stage's
+    work is filled in only when it is itself timed."""
+    sh = shape(ffn="swiglu", norm="rmsnorm")
+    cd = codec(64, k=8)
+    toks = wl.markov1_tokens(64, sh.vocab, 2)
+    log("profile mask", sh, cd)
+    with dl.Model(sh, max_chunk=64) as m:
+        enc = m.encoder(cd, toks)
+        m.profile(True, stages=["ffn_in", "reveal"])
+        enc.step()
+        p = m.profile_read()
+        assert p["ffn_in"][1] == sh.n_layers and p["ffn_in"][2] > 0
+        assert p["reveal"][1] == 1
+        for name, (ms, n, work) in p.items():
+            if name not in ("ffn_in", "reveal"):
+                assert n == 0 and ms == 0.0 and work == 0.0, name
+        m.profile(True)
+        enc.step()
+        p = m.profile_read()
+        assert all(p[s][1] > 0 for s in ("qkv", "attn", "oproj", "ffn_in", "ffn_out", "head", "cdf"))
+        assert p["cdf"][2] == 8 * (8.0 * sh.vocab + 4.0)
+        m.profile(False)
