@@ -173,6 +173,21 @@ __device__ __forceinline__ void epilogue_staged(f32x16 (&acc)[WM / 32][WN / 32],
   const int lane = tid & 63, lr = lane & 31, lg = lane >> 5;
   const int wr0 = wm * WM, wc0 = wn * WN;  // wave tile origin inside the block tile
   float* sf = reinterpret_cast<float*>(smem);
+  // RESIDUAL: the residual rows this thread updates in phase 2 are loaded
+  // first, so their latency hides under phase 1
+  constexpr int CPR4 = BN / 4, IT4 = BM * CPR4 / NT;  // float4 chunks per row / per thread
+  static_assert(BM * CPR4 % NT == 0, "fp32 chunks must split evenly over the threads");
+  const bool vec4 = (ea.ldo & 3) == 0;
+  float4 xres[EPI == EPI_RESIDUAL ? IT4 : 1];
+  if constexpr (EPI == EPI_RESIDUAL) {
+#pragma unroll
+    for (int it = 0; it < IT4; ++it) {
+      const int qi = tid + it * NT, row = qi / CPR4, c = (qi % CPR4) * 4;
+      const int grow = m0 + row, gcol = n0 + c;
+      if (grow < Mv && gcol + 4 <= N && vec4)
+        xres[it] = *reinterpret_cast<const float4*>((const float*)ea.out + (size_t)grow * ea.ldo + gcol);
+    }
+  }
   // the main loop's last barrier ends every read of the operand tiles
   if constexpr (EPI == EPI_STORE_F32 || EPI == EPI_RESIDUAL || EPI == EPI_GELU) {
 #pragma unroll
@@ -238,19 +253,19 @@ __device__ __forceinline__ void epilogue_staged(f32x16 (&acc)[WM / 32][WN / 32],
     }
   }
   __syncthreads();
-  // phase 2: 16-byte chunks
+  // phase 2: 16-byte chunks, a fixed number per thread
   if constexpr (EPI == EPI_STORE_F32 || EPI == EPI_RESIDUAL) {
-    constexpr int CPR = BN / 4;  // float4 chunks per row
-    for (int qi = tid; qi < BM * CPR; qi += NT) {
-      const int row = qi / CPR, c = (qi % CPR) * 4;
+#pragma unroll
+    for (int it = 0; it < IT4; ++it) {
+      const int qi = tid + it * NT, row = qi / CPR4, c = (qi % CPR4) * 4;
       const int grow = m0 + row, gcol = n0 + c;
       if (grow >= Mv) continue;
       float* dst = (float*)ea.out + (size_t)grow * ea.ldo + gcol;
       const float* src = sf + row * SE::PF + c;
-      if (gcol + 4 <= N && (ea.ldo & 3) == 0) {
+      if (gcol + 4 <= N && vec4) {
         float4 v = *reinterpret_cast<const float4*>(src);
         if constexpr (EPI == EPI_RESIDUAL) {
-          const float4 o = *reinterpret_cast<const float4*>(dst);
+          const float4 o = xres[it];
           v.x = o.x + v.x; v.y = o.y + v.y; v.z = o.z + v.z; v.w = o.w + v.w;
         }
         *reinterpret_cast<float4*>(dst) = v;
@@ -267,8 +282,10 @@ __device__ __forceinline__ void epilogue_staged(f32x16 (&acc)[WM / 32][WN / 32],
     constexpr int CPR = W / 8;
     const int gc0 = EPI == EPI_GELU ? n0 : n0 / 2;
     const int Nout = EPI == EPI_GELU ? N : N / 2;
-    for (int qi = tid; qi < BM * CPR; qi += NT) {
-      const int row = qi / CPR, c = (qi % CPR) * 8;
+    static_assert(BM * CPR % NT == 0, "bf16 chunks must split evenly over the threads");
+#pragma unroll
+    for (int it = 0; it < BM * CPR / NT; ++it) {
+      const int qi = tid + it * NT, row = qi / CPR, c = (qi % CPR) * 8;
       const int grow = m0 + row, gcol = gc0 + c;
       if (grow >= Mv) continue;
       bf16_t* dst = (bf16_t*)ea.out + (size_t)grow * ea.ldo + gcol;
@@ -285,8 +302,10 @@ __device__ __forceinline__ void epilogue_staged(f32x16 (&acc)[WM / 32][WN / 32],
     if (which < 2) {
       constexpr int CPR = BN / 8;
       bf16_t* base = (bf16_t*)(which == 0 ? ea.q : ea.k);
-      for (int qi = tid; qi < BM * CPR; qi += NT) {
-        const int row = qi / CPR, c = (qi % CPR) * 8;
+      static_assert(BM * CPR % NT == 0, "bf16 chunks must split evenly over the threads");
+#pragma unroll
+      for (int it = 0; it < BM * CPR / NT; ++it) {
+        const int qi = tid + it * NT, row = qi / CPR, c = (qi % CPR) * 8;
         const int grow = m0 + row;
         if (grow >= Mv) continue;
         const int b = grow / T, t = grow - b * T;
@@ -297,8 +316,10 @@ __device__ __forceinline__ void epilogue_staged(f32x16 (&acc)[WM / 32][WN / 32],
     } else {
       constexpr int CPC = BM / 8;  // chunks of 8 rows per column
       bf16_t* base = (bf16_t*)ea.vt;
-      for (int qi = tid; qi < BN * CPC; qi += NT) {
-        const int col = qi / CPC, r0 = (qi % CPC) * 8;
+      static_assert(BN * CPC % NT == 0, "bf16 chunks must split evenly over the threads");
+#pragma unroll
+      for (int it = 0; it < BN * CPC / NT; ++it) {
+        const int qi = tid + it * NT, col = qi / CPC, r0 = (qi % CPC) * 8;
         const int grow = m0 + r0;
         if (grow >= Mv) continue;
         const int h = (nb + col) / dh, dim = (nb + col) % dh;
