@@ -90,3 +90,71 @@ class RangeDecoder:
             self.D = (self.D << 8) | self._byte()
             self.range <<= 8
         return s
+
+
+# ---------------------------------------------------------------------------
+# rANS (range Asymmetric Numeral Systems, Duda 2013), the statistical coder
+# the paper adopts.  State x in [L, L * 2^32) with L = 2^31, 32-bit words, so
+# any P <= 31 works.  Coding a symbol with interval [start, start + f) of a
+# 2^P total maps x to floor(x / f) * 2^P + (x mod f) + start, after first
+# writing the low word of x while x >= (L >> P) * 2^32 * f.  rANS is last in,
+# first out: the encoder keeps the chunk's intervals and codes them in
+# reverse, so the decoder reads them in coding order.  Stream: the final
+# state as 8 little-endian bytes, then the 32-bit words in the order the
+# decoder consumes them (little-endian).  Decoding ends in state L; any other
+# end state is a corrupt stream.
+RANS_L = 1 << 31
+
+
+class RansEncoder:
+    def __init__(self, P: int):
+        if not 1 <= P <= 31:
+            raise ValueError("rANS needs 1 <= P <= 31")
+        self.P = P
+        self.intervals = []
+
+    def encode(self, start: int, freq: int) -> None:
+        if freq <= 0 or start < 0 or start + freq > (1 << self.P):
+            raise ValueError("bad symbol interval")
+        self.intervals.append((start, freq))
+
+    def finish(self) -> bytes:
+        x, words = RANS_L, []
+        for start, f in reversed(self.intervals):
+            x_max = ((RANS_L >> self.P) << 32) * f
+            while x >= x_max:
+                words.append(x & 0xFFFFFFFF)
+                x >>= 32
+            x = (x // f << self.P) + (x % f) + start
+        out = bytearray(x.to_bytes(8, "little"))
+        for w in reversed(words):
+            out += w.to_bytes(4, "little")
+        return bytes(out)
+
+
+class RansDecoder:
+    def __init__(self, data: bytes, P: int):
+        if len(data) < 8 or (len(data) - 8) % 4:
+            raise CorruptStream("rANS stream length")
+        self.data, self.P = data, P
+        self.x = int.from_bytes(data[:8], "little")
+        self.pos = 8
+        if not RANS_L <= self.x < (RANS_L << 32):
+            raise CorruptStream("rANS state out of range")
+
+    def decode(self, cdf) -> int:
+        mask = (1 << self.P) - 1
+        slot = self.x & mask
+        s = bisect.bisect_right(cdf, slot) - 1
+        lo, hi = int(cdf[s]), int(cdf[s + 1])
+        self.x = (hi - lo) * (self.x >> self.P) + slot - lo
+        while self.x < RANS_L:
+            if self.pos + 4 > len(self.data):
+                raise CorruptStream("rANS stream ended early")
+            self.x = (self.x << 32) | int.from_bytes(self.data[self.pos:self.pos + 4], "little")
+            self.pos += 4
+        return s
+
+    def done(self) -> bool:
+        """True when the stream is fully consumed and the state is back at L."""
+        return self.pos == len(self.data) and self.x == RANS_L

@@ -1,15 +1,19 @@
 """The iterative diffusion compression pipeline (Diffusion-Based Compression
 Pipeline section, Figure 1).
 
-Per window (chunk) of the input: start from the fully masked state S(0)
-(initial context c = 0), then repeat until no position is masked: one forward
-pass gives a distribution at every masked position; the commitment schedule
-picks positions; their true symbols are coded with their predicted (quantised)
-distributions in ascending position order; the symbols are revealed in the
-state.  Decoding replays exactly the same decisions from the header
-parameters alone.  Windows are non-overlapping and independent, so every
-chunk has its own coder state and bitstream; a final partial chunk is coded at
-its own length.
+Per window (chunk) of the input: start from the state S(0) in which every
+position is masked except the c initial-context positions (Initial Context
+Strategies; c = 0 is the fully masked start), then repeat until no position is
+masked: one forward pass gives a distribution at every masked position; the
+commitment schedule picks positions; their true symbols are coded with their
+predicted (quantised) distributions in ascending position order; the symbols
+are revealed in the state.  Decoding replays exactly the same decisions from
+the header parameters alone.  Windows are non-overlapping and independent, so
+every chunk has its own coder state and bitstream; a final partial chunk is
+coded at its own length.
+
+Chunk payload: the initial context (c little-endian u16 positions, ascending,
+then their c u32 symbols) followed by the coder's bytes.
 """
 from __future__ import annotations
 
@@ -19,10 +23,12 @@ from typing import List, Optional
 
 import numpy as np
 
+import workloads as wl
+
 from . import model as M
 from .cdf import cdf_row
-from .coder import RangeDecoder, RangeEncoder
-from .schedule import entropy_bits, select
+from .coder import CorruptStream, RangeDecoder, RangeEncoder, RansDecoder, RansEncoder
+from .schedule import block_sizes, entropy_bits, select
 
 
 @dataclass
@@ -41,14 +47,51 @@ def _pass(shape, W, state):
     return lg, pos, entropy_bits(lg)
 
 
-def encode_chunk(shape, W, tokens: np.ndarray, codec, forced: Optional[list] = None) -> ChunkResult:
+def context_positions(codec, T: int, chunk_index: int) -> np.ndarray:
+    """The chunk's initial-context positions (ascending): the first c, or the c
+    positions with the smallest seeded keys (seed context_seed + chunk index)."""
+    c = min(int(codec.context), T)
+    if c == 0:
+        return np.zeros(0, dtype=np.int64)
+    if codec.context_kind == "contiguous":
+        return np.arange(c, dtype=np.int64)
+    if codec.context_kind == "random":
+        perm = wl.seeded_permutation(codec.context_seed + chunk_index, T)
+        return np.sort(perm[:c])
+    raise ValueError(codec.context_kind)
+
+
+def _encoder(codec):
+    if codec.coder == "rans":
+        return RansEncoder(codec.cdf_bits)
+    return RangeEncoder(codec.coder_bits, codec.cdf_bits)
+
+
+def _decoder(codec, data: bytes):
+    if codec.coder == "rans":
+        return RansDecoder(data, codec.cdf_bits)
+    return RangeDecoder(data, codec.coder_bits, codec.cdf_bits)
+
+
+def _selection(codec, state, mask_id, pos, H, sizes, k):
+    if codec.schedule == "entropy":
+        return select(H, pos, codec.tau_bits, codec.m_min, codec.m_max)
+    masked = np.flatnonzero(state == mask_id)
+    return masked[: sizes[k]]
+
+
+def encode_chunk(shape, W, tokens: np.ndarray, codec, forced: Optional[list] = None,
+                 chunk_index: int = 0) -> ChunkResult:
     """Encode one chunk.  ``forced`` replays a given list of per-pass
     selections instead of the schedule's own (used to compare code lengths
     along another implementation's trajectory)."""
     tokens = np.asarray(tokens, dtype=np.int64)
     T = tokens.shape[0]
     state = np.full(T, shape.mask_id, dtype=np.int64)
-    enc = RangeEncoder(codec.coder_bits, codec.cdf_bits)
+    ctx = context_positions(codec, T, chunk_index)
+    state[ctx] = tokens[ctx]
+    sizes = None if codec.schedule == "entropy" else block_sizes(codec, T - len(ctx))
+    enc = _encoder(codec)
     res = ChunkResult(b"", 0)
     P = codec.cdf_bits
     while np.any(state == shape.mask_id):
@@ -58,7 +101,7 @@ def encode_chunk(shape, W, tokens: np.ndarray, codec, forced: Optional[list] = N
             if np.any(state[sel] != shape.mask_id) or len(sel) == 0:
                 raise ValueError("forced selection is not a set of masked positions")
         else:
-            sel = select(H, pos, codec.tau_bits, codec.m_min, codec.m_max)
+            sel = _selection(codec, state, shape.mask_id, pos, H, sizes, res.passes)
         row_of = {int(p): i for i, p in enumerate(pos)}
         for p in sel:
             row = lg[row_of[int(p)]]
@@ -73,22 +116,41 @@ def encode_chunk(shape, W, tokens: np.ndarray, codec, forced: Optional[list] = N
         res.entropies.append(H)
         state[sel] = tokens[sel]
         res.passes += 1
-    res.coded_bits = enc.code_length_bits()
-    res.payload = enc.finish()
+    head = ctx.astype("<u2").tobytes() + tokens[ctx].astype("<u4").tobytes()
+    if codec.coder == "rans":
+        body = enc.finish()
+        res.coded_bits = 8.0 * len(body)
+    else:
+        res.coded_bits = enc.code_length_bits()
+        body = enc.finish()
+    res.payload = head + body
     return res
 
 
 def decode_chunk(shape, W, payload: bytes, T: int, codec) -> np.ndarray:
+    c = min(int(codec.context), T)
+    if len(payload) < 6 * c:
+        raise CorruptStream("chunk shorter than its initial context")
+    ctx = np.frombuffer(payload[: 2 * c], dtype="<u2").astype(np.int64)
+    sym = np.frombuffer(payload[2 * c: 6 * c], dtype="<u4").astype(np.int64)
+    if np.any(ctx >= T) or np.any(np.diff(ctx) <= 0) or np.any(sym >= shape.vocab):
+        raise CorruptStream("bad initial context")
     state = np.full(T, shape.mask_id, dtype=np.int64)
-    dec = RangeDecoder(payload, codec.coder_bits, codec.cdf_bits)
+    state[ctx] = sym
+    sizes = None if codec.schedule == "entropy" else block_sizes(codec, T - c)
+    dec = _decoder(codec, payload[6 * c:])
     P = codec.cdf_bits
+    k = 0
     while np.any(state == shape.mask_id):
         lg, pos, H = _pass(shape, W, state)
-        sel = select(H, pos, codec.tau_bits, codec.m_min, codec.m_max)
+        sel = _selection(codec, state, shape.mask_id, pos, H, sizes, k)
         row_of = {int(p): i for i, p in enumerate(pos)}
         for p in sel:
             cdf = cdf_row(lg[row_of[int(p)]], P)
             state[p] = dec.decode(cdf)
+        k += 1
+    if codec.coder == "rans" and not dec.done():
+        raise CorruptStream("rANS stream did not end in its initial state")
     return state
 
 
@@ -97,7 +159,8 @@ def chunk_bounds(n: int, chunk_len: int):
 
 
 def encode(shape, W, tokens: np.ndarray, codec) -> List[ChunkResult]:
-    return [encode_chunk(shape, W, tokens[a:b], codec) for a, b in chunk_bounds(len(tokens), codec.chunk_len)]
+    return [encode_chunk(shape, W, tokens[a:b], codec, chunk_index=i)
+            for i, (a, b) in enumerate(chunk_bounds(len(tokens), codec.chunk_len))]
 
 
 def decode(shape, W, payloads: List[bytes], n: int, codec) -> np.ndarray:

@@ -10,8 +10,20 @@ is silent: entropy ties go to the lower position; at most m_max positions are
 committed (the m_max lowest); if fewer than m_min positions are still masked,
 all of them are committed; committed positions are coded in ascending position
 order.  The fixed-k rule is tau = -inf, m_min = m_max = k.
+
+Left-to-right block schedules (items 1 and 2) commit the next u_k still-masked
+positions in ascending order at pass k; they need no entropies.
+- Uniform block: u = floor(n / K) per pass over the n masked positions.  Where
+  the paper is silent: the remainder n mod K goes to the last block, and
+  K > n is read as K = n (one symbol per pass, the autoregressive order).
+- Progressive: u_k = round(u_1 r^(k-1)), rounding half up, with r^(k-1) formed
+  by repeated multiplication in fp64; every block holds at least one symbol
+  and the last one is cut to what remains.  With r = 1 and u_1 = n / K (K
+  dividing n) it is the uniform block schedule.
 """
 from __future__ import annotations
+
+import math
 
 import numpy as np
 
@@ -39,3 +51,35 @@ def select(H: np.ndarray, pos: np.ndarray, tau: float, m_min: int, m_max: int) -
     n = commit_count(H, tau, m_min, m_max)
     order = sorted(range(len(pos)), key=lambda i: (H[i], pos[i]))
     return np.sort(pos[order[:n]])
+
+
+def uniform_blocks(n: int, K: int) -> list:
+    """Block sizes u_1..u_K of the uniform block schedule over n positions."""
+    if n <= 0:
+        return []
+    K = max(1, min(K, n))
+    u = n // K
+    sizes = [u] * K
+    sizes[-1] += n - u * K
+    return sizes
+
+
+def progressive_blocks(n: int, u1: int, r: float) -> list:
+    """Block sizes of the progressive schedule over n positions."""
+    sizes, left, g = [], n, float(u1)
+    while left > 0:
+        u = max(1, int(math.floor(g + 0.5)))
+        u = min(u, left)
+        sizes.append(u)
+        left -= u
+        g = g * float(r)
+    return sizes
+
+
+def block_sizes(codec, n: int) -> list:
+    """Per-pass commit counts of a left-to-right block schedule."""
+    if codec.schedule == "uniform":
+        return uniform_blocks(n, codec.blocks)
+    if codec.schedule == "progressive":
+        return progressive_blocks(n, codec.u1, codec.growth)
+    raise ValueError(codec.schedule)

@@ -107,3 +107,62 @@ def test_range_decoder_rejects_out_of_range_target():
     dec = ORC.RangeDecoder(b"\xff" * 8, 32, 16)
     with pytest.raises(ORC.CorruptStream):
         dec.decode([0, 1, 1 << 16])
+
+
+# ---------------------------------------------------------------- rANS
+from oracle.coder import RANS_L, CorruptStream, RansDecoder, RansEncoder  # noqa: E402
+
+
+def _random_cdf(rng, V, P):
+    w = rng.random(V) ** 3 + 1e-9
+    f = 1 + (w / w.sum() * ((1 << P) - V)).astype(np.int64)
+    f[int(np.argmax(f))] += (1 << P) - int(f.sum())
+    return np.concatenate([[0], np.cumsum(f)]).astype(np.int64), f
+
+
+@pytest.mark.parametrize("P", [2, 16, 24, 31])
+def test_rans_roundtrip(P):
+    rng = np.random.default_rng(P)
+    for trial in range(10):
+        V = int(rng.integers(2, min(300, 1 << P) + 1))
+        cdf, f = _random_cdf(rng, V, P)
+        syms = rng.integers(0, V, size=int(rng.integers(0, 2000)))
+        enc = RansEncoder(P)
+        for s in syms:
+            enc.encode(int(cdf[s]), int(f[s]))
+        data = enc.finish()
+        dec = RansDecoder(data, P)
+        assert [dec.decode(cdf) for _ in syms] == list(syms)
+        assert dec.done()
+
+
+@pytest.mark.parametrize("P", [8, 16, 24])
+def test_rans_length_bound(P):
+    """Coded length minus the information I = sum log2(2^P / f) lies in
+    (32 - n d, 64 + n d]: the initial state L = 2^31 and the 64-bit flush
+    cost 95 - log2(x_final) bits with x_final in [2^31, 2^63), and each step
+    maps x to x 2^P / f within a factor (1 +- 2^(P-31)), d = -log2(1 - 2^(P-31))."""
+    rng = np.random.default_rng(100 + P)
+    d = -math.log2(1.0 - 2.0 ** (P - 31))
+    for trial in range(20):
+        V = int(rng.integers(2, min(500, 1 << P) + 1))
+        cdf, f = _random_cdf(rng, V, P)
+        syms = rng.integers(0, V, size=int(rng.integers(1, 4000)))
+        enc = RansEncoder(P)
+        info = 0.0
+        for s in syms:
+            enc.encode(int(cdf[s]), int(f[s]))
+            info += math.log2((1 << P) / f[s])
+        excess = 8 * len(enc.finish()) - info
+        n = len(syms)
+        assert 32 - n * d - 1e-9 < excess <= 64 + n * d + 1e-9, (trial, excess)
+
+
+def test_rans_empty_and_corrupt_streams():
+    data = RansEncoder(16).finish()
+    assert data == RANS_L.to_bytes(8, "little")      # no symbol: the initial state only
+    assert RansDecoder(data, 16).done()
+    with pytest.raises(CorruptStream):
+        RansDecoder(b"\x00" * 8, 16)                  # state below L
+    with pytest.raises(CorruptStream):
+        RansDecoder(data + b"\x01", 16)               # not a whole number of words

@@ -72,3 +72,62 @@ def test_wrong_payload_does_not_roundtrip():
     except ValueError:
         return
     assert not np.array_equal(dec, toks)
+
+
+# ------------------------------------------------- block schedules, rANS, initial context
+from oracle.coder import CorruptStream  # noqa: E402
+from oracle.schedule import block_sizes  # noqa: E402
+
+
+@pytest.mark.parametrize("codec_kw", [
+    dict(schedule="uniform", blocks=5),
+    dict(schedule="uniform", blocks=24),                  # autoregressive: one per pass
+    dict(schedule="progressive", u1=1, growth=1.7),
+    dict(schedule="uniform", blocks=3, coder="rans"),
+    dict(schedule="progressive", u1=2, growth=1.3, context=4, context_kind="random", context_seed=7),
+    dict(schedule="uniform", blocks=4, context=3, context_kind="contiguous", coder="rans"),
+    dict(m_min=3, m_max=3, context=5, context_kind="random", context_seed=1, coder="rans"),
+])
+def test_block_schedules_context_and_rans_roundtrip(codec_kw):
+    shape, W, codec = tiny(24, **codec_kw)
+    toks = wl.markov2_bytes(53, 11)
+    res = OD.encode(shape, W, toks, codec)
+    for i, ((a, b), r) in enumerate(zip(OD.chunk_bounds(53, 24), res)):
+        T = b - a
+        ctx = OD.context_positions(codec, T, i)
+        assert len(ctx) == min(codec.context, T) and len(set(ctx.tolist())) == len(ctx)
+        if codec.context_kind == "contiguous":
+            assert ctx.tolist() == list(range(len(ctx)))
+        rest = sorted(set(range(T)) - set(ctx.tolist()))
+        allsel = np.concatenate(r.selections) if r.selections else np.zeros(0, dtype=np.int64)
+        assert sorted(allsel.tolist()) == rest          # coverage of the masked positions
+        if codec.schedule != "entropy":
+            # left to right: the passes commit consecutive runs of the masked positions
+            assert allsel.tolist() == rest
+            assert [len(s) for s in r.selections] == block_sizes(codec, len(rest))
+    dec = OD.decode(shape, W, [r.payload for r in res], 53, codec)
+    assert np.array_equal(dec, toks)
+
+
+def test_autoregressive_special_case():
+    shape, W, codec = tiny(12, schedule="uniform", blocks=12)
+    toks = wl.markov2_bytes(12, 3)
+    (r,) = OD.encode(shape, W, toks, codec)
+    assert [s.tolist() for s in r.selections] == [[i] for i in range(12)]
+
+
+def test_full_context_chunk_stores_symbols_only():
+    shape, W, codec = tiny(10, context=16, coder="rans")
+    toks = wl.markov2_bytes(10, 4)
+    (r,) = OD.encode(shape, W, toks, codec)
+    assert r.passes == 0 and len(r.payload) == 6 * 10 + 8
+    assert np.array_equal(OD.decode(shape, W, [r.payload], 10, codec), toks)
+
+
+def test_rans_corrupt_tail_is_detected():
+    shape, W, codec = tiny(16, m_min=4, m_max=4, coder="rans")
+    toks = wl.markov2_bytes(16, 8)
+    (r,) = OD.encode(shape, W, toks, codec)
+    bad = r.payload[:-4]
+    with pytest.raises(CorruptStream):
+        OD.decode(shape, W, [bad], 16, codec)

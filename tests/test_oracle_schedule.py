@@ -132,3 +132,37 @@ def test_every_single_position_order_roundtrips_bruteforce():
         if list(order) == greedy:
             seen_greedy = True
     assert seen_greedy
+
+
+# ---------------------------------------------------------------- block schedules
+from oracle.schedule import progressive_blocks, uniform_blocks  # noqa: E402
+
+
+@pytest.mark.parametrize("n,K", [(10, 3), (2048, 16), (2048, 2048), (7, 1), (5, 9), (1, 1), (100, 7)])
+def test_uniform_blocks_cover_left_to_right(n, K):
+    sizes = uniform_blocks(n, K)
+    Ke = min(K, n)
+    assert sum(sizes) == n and len(sizes) == Ke
+    # floor(n / K) per pass, the remainder n mod K on the last block
+    assert all(u == n // Ke for u in sizes[:-1]) and sizes[-1] == n // Ke + n % Ke
+
+
+def test_uniform_blocks_special_cases():
+    assert uniform_blocks(0, 4) == []
+    assert uniform_blocks(9, 1) == [9]           # one-shot
+    assert uniform_blocks(6, 6) == [1] * 6       # autoregressive: one symbol per pass
+    assert uniform_blocks(3, 50) == [1, 1, 1]    # K > n read as K = n
+
+
+def test_progressive_blocks_hand_example():
+    # u1 = 2, r = 1.5: 2, 3 (2 * 1.5), round(4.5) = 5 (half up), round(6.75) = 7,
+    # then 10.125 is cut to the 3 positions left (20 = 2 + 3 + 5 + 7 + 3)
+    assert progressive_blocks(20, 2, 1.5) == [2, 3, 5, 7, 3]
+    # shrinking budgets never commit fewer than one symbol: 4, 2, 1, round(0.5) = 1, ...
+    assert progressive_blocks(10, 4, 0.5) == [4, 2, 1, 1, 1, 1]
+
+
+@pytest.mark.parametrize("n,K", [(12, 4), (2048, 16), (64, 64), (30, 1)])
+def test_progressive_with_unit_growth_is_uniform(n, K):
+    # Schedules, item 2: r = 1 reduces to the uniform block schedule
+    assert progressive_blocks(n, n // K, 1.0) == uniform_blocks(n, K)

@@ -71,10 +71,17 @@ class ModelShape:
 class CodecParams:
     """Commitment-schedule and coder parameters stored in the container header.
 
-    Entropy-based schedule (Symbol Commitment Schedules, item 3): commit every
-    masked position with H <= tau_bits; if fewer than m_min qualify commit the
-    m_min lowest-entropy ones.  m_max caps the count.  tau_bits = -inf gives
-    the fixed-k rule (m_min = m_max = k).
+    schedule (Symbol Commitment Schedules):
+      "entropy"     item 3: commit every masked position with H <= tau_bits; if
+                    fewer than m_min qualify commit the m_min lowest-entropy
+                    ones; m_max caps the count.  tau_bits = -inf gives the
+                    fixed-k rule (m_min = m_max = k).
+      "uniform"     item 1: ``blocks`` = K left-to-right blocks per chunk.
+      "progressive" item 2: left-to-right blocks of round(u1 * growth^(k-1)).
+    coder: "range" (W = coder_bits) or "rans" (64-bit state, 32-bit words).
+    context / context_kind (Initial Context Strategies): c symbols per chunk
+    left visible and stored in the container, the first c ("contiguous") or c
+    seeded-random positions ("random", seed context_seed + chunk index).
     """
     chunk_len: int
     tau_bits: float
@@ -83,6 +90,14 @@ class CodecParams:
     cdf_bits: int
     coder_bits: int
     batch: int = 1
+    schedule: str = "entropy"
+    blocks: int = 0
+    u1: int = 0
+    growth: float = 1.0
+    coder: str = "range"
+    context: int = 0
+    context_kind: str = "contiguous"
+    context_seed: int = 0
 
 
 def fan_in_exp(fan_in: int) -> int:
