@@ -83,14 +83,43 @@ typedef struct dlmc_model_config {
 typedef struct dlmc_codec_params {
   uint32_t struct_size; /* sizeof(dlmc_codec_params) */
   int32_t chunk_len;    /* window length w, 1..max_chunk */
+  /* entropy schedule (Symbol Commitment Schedules, item 3): commit every
+   * masked position with entropy <= tau_bits, at least m_min (the lowest),
+   * at most m_max; tau_bits = -inf with m_min = m_max = k is fixed-k.  For the
+   * block schedules m_max is the per-pass capacity (no block may exceed it). */
   float tau_bits;
   int32_t m_min; /* >= 1 */
   int32_t m_max; /* m_min..1024 */
-  int32_t cdf_bits;   /* P: CDF precision, 2^P > vocab, P <= coder_bits - 16 */
-  int32_t coder_bits; /* W: range coder width, 32 or 64 */
+  int32_t cdf_bits;   /* P: CDF precision, 2^P > vocab; range coder: P <= coder_bits - 16,
+                         rANS: P <= 31 */
+  int32_t coder_bits; /* W: range coder width, 32 or 64 (rANS: ignored, 64) */
   int32_t batch;      /* chunks per forward, 1..max_batch; does not change the output */
   int32_t flags;      /* DLMC_FLAG_* */
+  int32_t schedule;   /* DLMC_SCHED_* */
+  int32_t blocks;     /* uniform block schedule: K >= 1 blocks per chunk
+                         (item 1: u = floor(n/K) left to right, the remainder
+                         n mod K on the last block, K > n read as K = n) */
+  int32_t u1;         /* progressive schedule (item 2): first block >= 1 */
+  double growth;      /* progressive: ratio r > 0; u_k = round-half-up(u1 r^(k-1)),
+                         r^(k-1) by repeated fp64 multiplication, >= 1 per pass,
+                         the last block cut to what remains */
+  int32_t coder;      /* DLMC_CODER_* */
+  int32_t context;    /* initial context (Initial Context Strategies): c >= 0
+                         symbols per chunk left visible and stored in the chunk
+                         payload (min(c, chunk length) for a short chunk) */
+  int32_t context_kind; /* DLMC_CONTEXT_* */
+  int32_t reserved;     /* 0 */
+  uint64_t context_seed; /* random context of chunk i: the c positions with the
+                            smallest keys splitmix64(splitmix64(seed + i) + p) */
 } dlmc_codec_params;
+
+#define DLMC_SCHED_ENTROPY 0
+#define DLMC_SCHED_UNIFORM 1
+#define DLMC_SCHED_PROGRESSIVE 2
+#define DLMC_CODER_RANGE 0
+#define DLMC_CODER_RANS 1
+#define DLMC_CONTEXT_CONTIGUOUS 0 /* the first c positions */
+#define DLMC_CONTEXT_RANDOM 1     /* c seeded-random positions */
 
 #define DLMC_FLAG_CRC 1 /* store and check a CRC-32 of every chunk's tokens */
 
@@ -218,6 +247,13 @@ dlmc_status dlmc_rc_encode(const uint32_t* start, const uint32_t* freq, uint64_t
 /* Decode n symbols, symbol i with host cdf[i*(V+1) .. i*(V+1)+V]. */
 dlmc_status dlmc_rc_decode(const uint8_t* in, uint64_t len, const uint32_t* cdf, uint64_t n,
                            int32_t V, int32_t cdf_bits, int32_t coder_bits, int32_t* sym);
+/* rANS (the stream of a DLMC_CODER_RANS chunk payload after its context):
+ * code n intervals, 1 <= P <= 31; decoding checks that the stream ends in
+ * the coder's initial state (E_CORRUPT otherwise). */
+dlmc_status dlmc_rans_encode(const uint32_t* start, const uint32_t* freq, uint64_t n,
+                             int32_t cdf_bits, uint8_t* out, uint64_t cap, uint64_t* out_len);
+dlmc_status dlmc_rans_decode(const uint8_t* in, uint64_t len, const uint32_t* cdf, uint64_t n,
+                             int32_t V, int32_t cdf_bits, int32_t* sym);
 
 /* ---- errors -------------------------------------------------------------- */
 const char* dlmc_status_string(dlmc_status s);

@@ -55,7 +55,16 @@ class CodecParams(ctypes.Structure):
                 ("tau_bits", ctypes.c_float), ("m_min", ctypes.c_int32),
                 ("m_max", ctypes.c_int32), ("cdf_bits", ctypes.c_int32),
                 ("coder_bits", ctypes.c_int32), ("batch", ctypes.c_int32),
-                ("flags", ctypes.c_int32)]
+                ("flags", ctypes.c_int32), ("schedule", ctypes.c_int32),
+                ("blocks", ctypes.c_int32), ("u1", ctypes.c_int32),
+                ("growth", ctypes.c_double), ("coder", ctypes.c_int32),
+                ("context", ctypes.c_int32), ("context_kind", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("context_seed", ctypes.c_uint64)]
+
+
+SCHEDULE = {"entropy": 0, "uniform": 1, "progressive": 2}
+CODER = {"range": 0, "rans": 1}
+CONTEXT = {"contiguous": 0, "random": 1}
 
 
 TRACE_FN = ctypes.CFUNCTYPE(None, ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint64,
@@ -86,6 +95,8 @@ _SIGS = {
     "dlmc_profile_read": (i32, [vp, i32, P(ctypes.c_double), P(u64), P(ctypes.c_double)]),
     "dlmc_rc_encode": (i32, [vp, vp, u64, i32, i32, vp, u64, P(u64)]),
     "dlmc_rc_decode": (i32, [vp, u64, vp, u64, i32, i32, i32, vp]),
+    "dlmc_rans_encode": (i32, [vp, vp, u64, i32, vp, u64, P(u64)]),
+    "dlmc_rans_decode": (i32, [vp, u64, vp, u64, i32, i32, vp]),
     "dlmc_status_string": (ctypes.c_char_p, [i32]),
     "dlmc_last_error": (ctypes.c_char_p, []),
 }
@@ -137,7 +148,10 @@ def model_config(shape, max_chunk: int, max_batch: int) -> ModelConfig:
 def codec_params(codec, batch: Optional[int] = None, crc: bool = False) -> CodecParams:
     return CodecParams(ctypes.sizeof(CodecParams), codec.chunk_len, codec.tau_bits, codec.m_min,
                        codec.m_max, codec.cdf_bits, codec.coder_bits,
-                       codec.batch if batch is None else batch, FLAG_CRC if crc else 0)
+                       codec.batch if batch is None else batch, FLAG_CRC if crc else 0,
+                       SCHEDULE[codec.schedule], codec.blocks, codec.u1, float(codec.growth),
+                       CODER[codec.coder], codec.context, CONTEXT[codec.context_kind], 0,
+                       codec.context_seed)
 
 
 class Encoder:
@@ -355,4 +369,25 @@ def rc_decode(data: bytes, cdfs: np.ndarray, cdf_bits: int, coder_bits: int) -> 
     out = np.empty(max(n, 1), dtype=np.int32)
     _check(lib().dlmc_rc_decode(_ptr(buf), len(buf), _ptr(c), n, V1 - 1, cdf_bits, coder_bits,
                                 _ptr(out)))
+    return out[:n]
+
+
+def rans_encode(start, freq, cdf_bits: int) -> bytes:
+    s = np.ascontiguousarray(start, dtype=np.uint32)
+    f = np.ascontiguousarray(freq, dtype=np.uint32)
+    cap = len(s) * 4 + 16
+    out = np.empty(cap, dtype=np.uint8)
+    n = u64(0)
+    _check(lib().dlmc_rans_encode(_ptr(s), _ptr(f), len(s), cdf_bits, _ptr(out), cap,
+                                  ctypes.byref(n)))
+    return out[: n.value].tobytes()
+
+
+def rans_decode(data: bytes, cdfs: np.ndarray, cdf_bits: int) -> np.ndarray:
+    c = np.ascontiguousarray(cdfs, dtype=np.uint32)
+    n, V1 = c.shape
+    buf = np.frombuffer(data, dtype=np.uint8).copy()
+    out = np.empty(max(n, 1), dtype=np.int32)
+    _check(lib().dlmc_rans_decode(_ptr(buf) if len(buf) else None, len(buf), _ptr(c), n, V1 - 1,
+                                  cdf_bits, _ptr(out)))
     return out[:n]

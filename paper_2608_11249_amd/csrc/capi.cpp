@@ -347,6 +347,42 @@ dlmc_status dlmc_rc_decode(const uint8_t* in, uint64_t len, const uint32_t* cdf,
   });
 }
 
+dlmc_status dlmc_rans_encode(const uint32_t* start, const uint32_t* freq, uint64_t n,
+                             int32_t cdf_bits, uint8_t* out, uint64_t cap, uint64_t* out_len) {
+  std::vector<uint8_t> bytes;
+  dlmc_status st = guard([&] {
+    DLMC_CHECK(cdf_bits >= 1 && cdf_bits <= 31, DLMC_E_INVAL, "rANS needs 1 <= cdf_bits <= 31");
+    DLMC_CHECK(n == 0 || (start && freq), DLMC_E_INVAL, "NULL argument");
+    RansEncoder enc;
+    enc.reset(cdf_bits);
+    for (uint64_t i = 0; i < n; ++i) {
+      DLMC_CHECK(freq[i] >= 1 && (uint64_t)start[i] + freq[i] <= (1ull << cdf_bits), DLMC_E_INVAL,
+                 "bad symbol interval");
+      enc.encode(start[i], freq[i]);
+    }
+    bytes = enc.finish();
+  });
+  if (st != DLMC_OK) return st;
+  return write_out(bytes, out, cap, out_len);
+}
+
+dlmc_status dlmc_rans_decode(const uint8_t* in, uint64_t len, const uint32_t* cdf, uint64_t n,
+                             int32_t V, int32_t cdf_bits, int32_t* sym) {
+  return guard([&] {
+    DLMC_CHECK(cdf_bits >= 1 && cdf_bits <= 31, DLMC_E_INVAL, "rANS needs 1 <= cdf_bits <= 31");
+    DLMC_CHECK(n == 0 || (cdf && sym && V >= 1), DLMC_E_INVAL, "NULL argument");
+    DLMC_CHECK(in || len == 0, DLMC_E_INVAL, "NULL stream");
+    RansDecoder dec;
+    if (!dec.reset(in, len, cdf_bits)) throw Error(DLMC_E_CORRUPT, "not an rANS stream");
+    for (uint64_t i = 0; i < n; ++i) {
+      const int s = dec.decode(cdf + i * ((uint64_t)V + 1), V);
+      if (s < 0) throw Error(DLMC_E_CORRUPT, "rANS stream corrupt");
+      sym[i] = s;
+    }
+    if (!dec.done()) throw Error(DLMC_E_CORRUPT, "rANS stream did not end in its initial state");
+  });
+}
+
 const char* dlmc_status_string(dlmc_status s) {
   switch (s) {
     case DLMC_OK: return "ok";

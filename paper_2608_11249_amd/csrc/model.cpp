@@ -269,7 +269,7 @@ uint64_t dlmc_model::hash() const {
 }
 
 void dlmc_model::forward(const int32_t* st_dev, int B, int T, float* logits_out, int32_t* rows_out,
-                         int32_t* n_rows_out, int64_t rows_hint) {
+                         int32_t* n_rows_out, int64_t rows_hint, bool rows_given) {
   DLMC_CHECK(B >= 1 && B <= cfg.max_batch && T >= 1 && T <= cfg.max_chunk, DLMC_E_INVAL,
              "batch / chunk length exceed the model's workspace");
   const int d = cfg.d_model, F = cfg.d_ffn, V = cfg.vocab, H = cfg.n_heads;
@@ -370,8 +370,8 @@ void dlmc_model::forward(const int32_t* st_dev, int B, int T, float* logits_out,
       }
     }
   }
-  // masked rows only: compaction, final norm gathered, LM head
-  {
+  // masked (or given) rows only: compaction, final norm gathered, LM head
+  if (!rows_given) {
     StageTimer t(this, DLMC_STAGE_COMPACT, Md * 8.0);
     compact_masked(s, st_dev, B, T, V, rw, nr, chunk_off, chunk_cnt);
   }

@@ -7,6 +7,7 @@
 
 #include "kernels.h"
 #include "range_coder.h"
+#include "rans_coder.h"
 
 struct dlmc_model {
   dlmc_model_config cfg{};
@@ -76,9 +77,11 @@ struct dlmc_model {
   void ensure_tokens(size_t n);
   uint64_t hash() const;
   // One forward pass over state[B*T] (device): logits at masked rows into
-  // logits_out (or the internal buffer), row ids and count likewise.
+  // logits_out (or the internal buffer), row ids and count likewise.  With
+  // rows_given the head rows are the ones already in rows / n_rows (the
+  // committed rows of a block schedule) instead of the masked rows.
   void forward(const int32_t* state, int B, int T, float* logits_out, int32_t* rows_out,
-               int32_t* n_rows_out, int64_t rows_hint = -1);
+               int32_t* n_rows_out, int64_t rows_hint = -1, bool rows_given = false);
 };
 
 namespace dlmc {
@@ -131,6 +134,13 @@ struct dlmc_session {
   std::vector<int> slot_left, slot_pass;
   std::vector<dlmc::RangeEncoder> encs;
   std::vector<dlmc::RangeDecoder> decs;
+  std::vector<dlmc::RansEncoder> rencs;
+  std::vector<dlmc::RansDecoder> rdecs;
+  // initial context and left-to-right block schedules
+  std::vector<std::vector<int32_t>> slot_ctx_pos, slot_ctx_sym;  // per slot
+  std::vector<std::vector<int32_t>> slot_order;  // masked positions, ascending
+  std::vector<int> slot_cursor;                  // next index into slot_order
+  std::vector<int> blocks;                       // block sizes of the current phase
   bool started = false;
   uint64_t passes = 0;
 
@@ -142,6 +152,11 @@ struct dlmc_session {
   uint32_t* h_cdf = nullptr;  // decode / trace: sel_cap * (V+1) per slot
   int32_t* h_dec = nullptr;
   int64_t* h_base = nullptr;
+  int32_t* h_state = nullptr;   // max_batch * max_chunk: a slot's initial state
+  int32_t* h_rows = nullptr;    // block schedules: head rows, selections, counts
+  int32_t* h_selpos = nullptr;
+  int32_t* h_selrow = nullptr;
+  int32_t* h_nsel_up = nullptr;
 
   ~dlmc_session();
   void begin_phase();

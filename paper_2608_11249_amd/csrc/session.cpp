@@ -1,10 +1,14 @@
 // The iterative diffusion compression pipeline (Diffusion-Based Compression
-// Pipeline section): every chunk starts fully masked (no initial context) and
-// each pass runs forward -> entropy -> schedule -> CDF -> code -> reveal until
-// no position is masked.  Chunks are independent windows; up to `batch` of
-// them share a forward pass, and a slot whose chunk is done takes the next one.
-// Every kernel computes a chunk's values independently of the other chunks in
-// the batch, so the batch size does not change the output.
+// Pipeline section): every chunk starts masked except for its initial context
+// (Initial Context Strategies; none by default) and each pass runs
+// forward -> schedule -> CDF -> code -> reveal until no position is masked.
+// The entropy schedule computes entropies at every masked row and selects on
+// the GPU; the left-to-right block schedules (uniform, progressive) know their
+// positions in advance, so only the committed rows go through the LM head.
+// Chunks are independent windows; up to `batch` of them share a forward pass,
+// and a slot whose chunk is done takes the next one.  Every kernel computes a
+// chunk's values independently of the other chunks in the batch, so the
+// batch size does not change the output.
 #include <cmath>
 #include <cstring>
 
@@ -15,8 +19,8 @@ using namespace dlmc;
 namespace {
 
 constexpr uint32_t MAGIC = 0x434D4C44u;  // "DLMC" little endian
-constexpr uint32_t VERSION = 1;
-constexpr size_t FIXED_HEADER = 80;
+constexpr uint32_t VERSION = 2;
+constexpr size_t FIXED_HEADER = 112;
 
 template <typename T>
 void put(std::vector<uint8_t>& v, size_t off, T x) {
@@ -46,13 +50,83 @@ void validate_codec(const dlmc_model* m, const dlmc_codec_params& c) {
              "chunk_len must be in 1..max_chunk");
   DLMC_CHECK(c.m_min >= 1 && c.m_max >= c.m_min && c.m_max <= 1024, DLMC_E_INVAL,
              "need 1 <= m_min <= m_max <= 1024");
-  DLMC_CHECK(c.coder_bits == 32 || c.coder_bits == 64, DLMC_E_INVAL, "coder_bits must be 32 or 64");
-  DLMC_CHECK(c.cdf_bits >= 2 && c.cdf_bits <= c.coder_bits - 16 && c.cdf_bits <= 31 &&
-                 (1ll << c.cdf_bits) > m->cfg.vocab,
-             DLMC_E_INVAL, "need vocab < 2^cdf_bits and cdf_bits <= coder_bits - 16");
+  DLMC_CHECK(c.coder == DLMC_CODER_RANGE || c.coder == DLMC_CODER_RANS, DLMC_E_INVAL, "unknown coder");
+  if (c.coder == DLMC_CODER_RANGE) {
+    DLMC_CHECK(c.coder_bits == 32 || c.coder_bits == 64, DLMC_E_INVAL, "coder_bits must be 32 or 64");
+    DLMC_CHECK(c.cdf_bits >= 2 && c.cdf_bits <= c.coder_bits - 16 && (1ll << c.cdf_bits) > m->cfg.vocab,
+               DLMC_E_INVAL, "need vocab < 2^cdf_bits and cdf_bits <= coder_bits - 16");
+  } else {
+    DLMC_CHECK(c.cdf_bits >= 2 && c.cdf_bits <= 31 && (1ll << c.cdf_bits) > m->cfg.vocab,
+               DLMC_E_INVAL, "rANS needs vocab < 2^cdf_bits and cdf_bits <= 31");
+  }
+  DLMC_CHECK(c.schedule >= DLMC_SCHED_ENTROPY && c.schedule <= DLMC_SCHED_PROGRESSIVE, DLMC_E_INVAL,
+             "unknown schedule");
+  DLMC_CHECK(c.schedule != DLMC_SCHED_UNIFORM || c.blocks >= 1, DLMC_E_INVAL,
+             "uniform block schedule needs blocks >= 1");
+  DLMC_CHECK(c.schedule != DLMC_SCHED_PROGRESSIVE ||
+                 (c.u1 >= 1 && std::isfinite(c.growth) && c.growth > 0.0),
+             DLMC_E_INVAL, "progressive schedule needs u1 >= 1 and a finite growth > 0");
+  DLMC_CHECK(c.context >= 0 && c.context <= 8192, DLMC_E_INVAL, "context must be in 0..8192");
+  DLMC_CHECK(c.context_kind == DLMC_CONTEXT_CONTIGUOUS || c.context_kind == DLMC_CONTEXT_RANDOM,
+             DLMC_E_INVAL, "unknown context kind");
+  DLMC_CHECK(c.reserved == 0, DLMC_E_INVAL, "reserved field must be 0");
   DLMC_CHECK(c.batch >= 1 && c.batch <= m->cfg.max_batch, DLMC_E_INVAL, "batch must be in 1..max_batch");
   DLMC_CHECK(!std::isnan(c.tau_bits), DLMC_E_INVAL, "tau_bits is NaN");
   DLMC_CHECK((c.flags & ~DLMC_FLAG_CRC) == 0, DLMC_E_INVAL, "unknown flags");
+}
+
+// Per-pass commit counts of a left-to-right block schedule over n masked
+// positions (Symbol Commitment Schedules, items 1 and 2).
+std::vector<int> block_sizes(const dlmc_codec_params& c, int n) {
+  std::vector<int> out;
+  if (n <= 0) return out;
+  if (c.schedule == DLMC_SCHED_UNIFORM) {
+    const int K = std::max(1, std::min(c.blocks, n));
+    const int u = n / K;
+    out.assign(K, u);
+    out.back() += n - u * K;
+  } else {
+    int left = n;
+    double g = (double)c.u1;
+    while (left > 0) {
+      const double r = std::floor(g + 0.5);  // round half up
+      const int u = r >= (double)left ? left : std::max(1, (int)r);
+      out.push_back(u);
+      left -= u;
+      g *= c.growth;
+    }
+  }
+  return out;
+}
+
+namespace {
+// splitmix64 (Steele, Lea and Flood, OOPSLA 2014)
+uint64_t splitmix64(uint64_t x) {
+  uint64_t z = x + 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+}  // namespace
+
+// Initial-context positions of chunk `chunk` (ascending): the first c, or the
+// c positions with the smallest keys splitmix64(splitmix64(seed + chunk) + p)
+// (ties by position).
+std::vector<int32_t> context_positions(const dlmc_codec_params& c, int T, uint64_t chunk) {
+  const int cc = std::min(c.context, T);
+  std::vector<int32_t> pos(cc);
+  if (cc == 0) return pos;
+  if (c.context_kind == DLMC_CONTEXT_CONTIGUOUS) {
+    for (int j = 0; j < cc; ++j) pos[j] = j;
+    return pos;
+  }
+  const uint64_t base = splitmix64(c.context_seed + chunk);
+  std::vector<std::pair<uint64_t, int32_t>> keys(T);
+  for (int p = 0; p < T; ++p) keys[p] = {splitmix64(base + (uint64_t)p), p};
+  std::partial_sort(keys.begin(), keys.begin() + cc, keys.end());
+  for (int j = 0; j < cc; ++j) pos[j] = keys[j].second;
+  std::sort(pos.begin(), pos.end());
+  return pos;
 }
 
 }  // namespace dlmc
@@ -65,20 +139,66 @@ dlmc_session::~dlmc_session() {
   (void)hipHostFree(h_cdf);
   (void)hipHostFree(h_dec);
   (void)hipHostFree(h_base);
+  (void)hipHostFree(h_state);
+  (void)hipHostFree(h_rows);
+  (void)hipHostFree(h_selpos);
+  (void)hipHostFree(h_selrow);
+  (void)hipHostFree(h_nsel_up);
 }
 
 void dlmc_session::assign(int b, uint64_t chunk) {
+  const int V = m->cfg.vocab, P = cp.cdf_bits;
+  const bool rans = cp.coder == DLMC_CODER_RANS;
   slot_chunk[b] = (int64_t)chunk;
-  slot_left[b] = T;
   slot_pass[b] = 0;
+  slot_cursor[b] = 0;
   h_base[b] = (int64_t)(chunk * (uint64_t)cp.chunk_len);
+  const int c = std::min(cp.context, T);
+  auto& cpos = slot_ctx_pos[b];
+  auto& csym = slot_ctx_sym[b];
   if (encode) {
-    encs[b].reset(cp.coder_bits, cp.cdf_bits);
+    cpos = context_positions(cp, T, chunk);
+    csym.resize(c);
+    for (int j = 0; j < c; ++j) csym[j] = tokens[(size_t)h_base[b] + cpos[j]];
+    if (rans) rencs[b].reset(P);
+    else encs[b].reset(cp.coder_bits, P);
   } else {
     const auto& p = payload[chunk];
-    decs[b].reset(p.data(), p.size(), cp.coder_bits, cp.cdf_bits);
+    DLMC_CHECK(p.size() >= (size_t)6 * c, DLMC_E_CORRUPT, "chunk shorter than its initial context");
+    cpos.resize(c);
+    csym.resize(c);
+    for (int j = 0; j < c; ++j) {
+      cpos[j] = get<uint16_t>(p.data(), 2 * (size_t)j);
+      csym[j] = (int32_t)get<uint32_t>(p.data(), 2 * (size_t)c + 4 * (size_t)j);
+      DLMC_CHECK(cpos[j] < T && (j == 0 || cpos[j] > cpos[j - 1]) && csym[j] >= 0 && csym[j] < V,
+                 DLMC_E_CORRUPT, "bad initial context");
+      tokens[(size_t)h_base[b] + cpos[j]] = csym[j];
+    }
+    const uint8_t* data = p.data() + 6 * (size_t)c;
+    const size_t len = p.size() - 6 * (size_t)c;
+    if (rans) {
+      if (!rdecs[b].reset(data, len, P)) throw Error(DLMC_E_CORRUPT, "not an rANS stream");
+    } else {
+      decs[b].reset(data, len, cp.coder_bits, P);
+    }
   }
-  fill_i32(m->stream, m->state + (size_t)b * T, m->cfg.vocab, (size_t)T);
+  slot_left[b] = T - c;
+  // initial state: [MASK] except the context symbols
+  int32_t* hs = h_state + (size_t)b * m->cfg.max_chunk;
+  std::fill(hs, hs + T, V);
+  for (int j = 0; j < c; ++j) hs[cpos[j]] = csym[j];
+  DLMC_HIP(hipMemcpyAsync(m->state + (size_t)b * T, hs, (size_t)T * 4, hipMemcpyHostToDevice, m->stream));
+  if (cp.schedule != DLMC_SCHED_ENTROPY) {
+    auto& ord = slot_order[b];
+    ord.clear();
+    for (int p = 0, j = 0; p < T; ++p) {
+      if (j < c && cpos[j] == p) {
+        ++j;
+        continue;
+      }
+      ord.push_back(p);
+    }
+  }
 }
 
 void dlmc_session::begin_phase() {
@@ -103,8 +223,15 @@ void dlmc_session::begin_phase() {
   slot_chunk.assign(B, -1);
   slot_left.assign(B, 0);
   slot_pass.assign(B, 0);
+  slot_cursor.assign(B, 0);
+  slot_ctx_pos.assign(B, {});
+  slot_ctx_sym.assign(B, {});
+  slot_order.assign(B, {});
   encs.assign(B, RangeEncoder());
   decs.assign(B, RangeDecoder());
+  rencs.assign(B, RansEncoder());
+  rdecs.assign(B, RansDecoder());
+  if (cp.schedule != DLMC_SCHED_ENTROPY) blocks = block_sizes(cp, T - std::min(cp.context, T));
   const uint64_t end = phase == 0 ? n_full : n_chunks;
   for (int b = 0; b < B; ++b) {
     if (next_chunk < end) {
@@ -129,15 +256,44 @@ int dlmc_session::step(uint64_t* coded) {
   int64_t masked = 0;  // masked positions before this pass (host bookkeeping)
   for (int b = 0; b < B; ++b)
     if (slot_chunk[b] >= 0) masked += slot_left[b];
-  m->forward(m->state, B, T, nullptr, nullptr, nullptr, masked);
-  {
-    StageTimer t(m, DLMC_STAGE_ENTROPY, (double)masked * V * 4.0);
-    entropy_rows(s, m->logits, B * T, m->n_rows, V, m->H, m->mx);
-  }
-  {
-    StageTimer t(m, DLMC_STAGE_SELECT, (double)masked * 8.0);
-    select_positions(s, m->H, m->rows, m->chunk_off, m->chunk_cnt, B, T, cp.tau_bits, cp.m_min, mm,
-                     m->sel_pos, m->sel_row, m->n_sel, m->err);
+  if (cp.schedule == DLMC_SCHED_ENTROPY) {
+    m->forward(m->state, B, T, nullptr, nullptr, nullptr, masked);
+    {
+      StageTimer t(m, DLMC_STAGE_ENTROPY, (double)masked * V * 4.0);
+      entropy_rows(s, m->logits, B * T, m->n_rows, V, m->H, m->mx);
+    }
+    {
+      StageTimer t(m, DLMC_STAGE_SELECT, (double)masked * 8.0);
+      select_positions(s, m->H, m->rows, m->chunk_off, m->chunk_cnt, B, T, cp.tau_bits, cp.m_min, mm,
+                       m->sel_pos, m->sel_row, m->n_sel, m->err);
+    }
+  } else {
+    // the next block of each slot's masked positions, in ascending order
+    int r = 0;
+    for (int b = 0; b < B; ++b) {
+      h_nsel_up[b] = 0;
+      if (slot_chunk[b] < 0 || slot_left[b] == 0) continue;
+      const int u = blocks[(size_t)slot_pass[b]];
+      for (int j = 0; j < u; ++j) {
+        const int pos = slot_order[b][(size_t)slot_cursor[b] + j];
+        h_selpos[b * mm + j] = pos;
+        h_selrow[b * mm + j] = r;
+        h_rows[r++] = b * T + pos;
+      }
+      h_nsel_up[b] = u;
+    }
+    h_nsel_up[B] = r;
+    DLMC_HIP(hipMemcpyAsync(m->rows, h_rows, (size_t)std::max(r, 1) * 4, hipMemcpyHostToDevice, s));
+    DLMC_HIP(hipMemcpyAsync(m->n_rows, h_nsel_up + B, 4, hipMemcpyHostToDevice, s));
+    DLMC_HIP(hipMemcpyAsync(m->sel_pos, h_selpos, (size_t)B * mm * 4, hipMemcpyHostToDevice, s));
+    DLMC_HIP(hipMemcpyAsync(m->sel_row, h_selrow, (size_t)B * mm * 4, hipMemcpyHostToDevice, s));
+    DLMC_HIP(hipMemcpyAsync(m->n_sel, h_nsel_up, (size_t)B * 4, hipMemcpyHostToDevice, s));
+    m->forward(m->state, B, T, nullptr, nullptr, nullptr, r, true);
+    {
+      // row statistics (the maximum feeds the CDF) at the committed rows only
+      StageTimer t(m, DLMC_STAGE_ENTROPY, (double)r * V * 4.0);
+      entropy_rows(s, m->logits, B * T, m->n_rows, V, m->H, m->mx);
+    }
   }
   const size_t cdf_rec = m->prof_recs.size();
   {
@@ -185,10 +341,13 @@ int dlmc_session::step(uint64_t* coded) {
     for (int j = 0; j < ns; ++j) {
       const int pos = h_pos[b * mm + j];
       if (encode) {
-        encs[b].encode(h_sym[2 * (b * mm + j)], h_sym[2 * (b * mm + j) + 1]);
+        const uint32_t st = h_sym[2 * (b * mm + j)], fr = h_sym[2 * (b * mm + j) + 1];
+        if (cp.coder == DLMC_CODER_RANS) rencs[b].encode(st, fr);
+        else encs[b].encode(st, fr);
       } else {
-        const int sym = decs[b].decode(rows_cdf + (size_t)j * row_words, V);
-        if (sym < 0) throw Error(DLMC_E_CORRUPT, "range decoder target out of range");
+        const uint32_t* cdf_j = rows_cdf + (size_t)j * row_words;
+        const int sym = cp.coder == DLMC_CODER_RANS ? rdecs[b].decode(cdf_j, V) : decs[b].decode(cdf_j, V);
+        if (sym < 0) throw Error(DLMC_E_CORRUPT, "decoder target out of range");
         tokens[base + pos] = sym;
         h_dec[b * mm + j] = sym;
         any_dec = true;
@@ -204,6 +363,7 @@ int dlmc_session::step(uint64_t* coded) {
     if (coded) *coded += (uint64_t)ns;
     slot_left[b] -= ns;
     slot_pass[b] += 1;
+    slot_cursor[b] += ns;
     DLMC_CHECK(slot_left[b] >= 0 && (ns > 0 || slot_left[b] == 0), DLMC_E_CORRUPT,
                "schedule committed no position");
   }
@@ -221,8 +381,22 @@ int dlmc_session::step(uint64_t* coded) {
     if (slot_left[b] == 0) {
       const uint64_t chunk = (uint64_t)slot_chunk[b];
       if (encode) {
-        payload[chunk] = encs[b].finish();
-      } else if (cp.flags & DLMC_FLAG_CRC) {
+        // chunk payload: the initial context (u16 positions, u32 symbols), then the coder's bytes
+        const auto& cpos = slot_ctx_pos[b];
+        const auto& csym = slot_ctx_sym[b];
+        const size_t c = cpos.size();
+        std::vector<uint8_t> body = cp.coder == DLMC_CODER_RANS ? rencs[b].finish() : encs[b].finish();
+        std::vector<uint8_t> pl(6 * c + body.size());
+        for (size_t j = 0; j < c; ++j) {
+          put<uint16_t>(pl, 2 * j, (uint16_t)cpos[j]);
+          put<uint32_t>(pl, 2 * c + 4 * j, (uint32_t)csym[j]);
+        }
+        if (!body.empty()) std::memcpy(pl.data() + 6 * c, body.data(), body.size());
+        payload[chunk] = std::move(pl);
+      } else if (cp.coder == DLMC_CODER_RANS && !rdecs[b].done()) {
+        throw Error(DLMC_E_CORRUPT, "rANS stream did not end in its initial state");
+      }
+      if (!encode && (cp.flags & DLMC_FLAG_CRC)) {
         const uint64_t base = chunk * (uint64_t)cp.chunk_len;
         const int len = phase == 0 ? cp.chunk_len : last_len;
         if (crc32(&tokens[base], (size_t)len * 4) != crc[chunk])
@@ -269,6 +443,13 @@ std::vector<uint8_t> dlmc_session::container() const {
   put<int32_t>(out, 64, cp.m_max);
   put<float>(out, 68, cp.tau_bits);
   put<int32_t>(out, 72, cp.batch);
+  put<int32_t>(out, 76, cp.schedule);
+  put<int32_t>(out, 80, cp.blocks);
+  put<int32_t>(out, 84, cp.u1);
+  put<double>(out, 88, cp.growth);
+  put<int32_t>(out, 96, cp.coder);
+  put<int32_t>(out, 100, cp.context);
+  put<int32_t>(out, 104, cp.context_kind);
   uint64_t off = 0;
   for (uint64_t c = 0; c <= n_chunks; ++c) {
     put<uint64_t>(out, FIXED_HEADER + c * 8, off);
@@ -307,6 +488,19 @@ static void session_common(dlmc_session* s, dlmc_model* m, const dlmc_codec_para
   pinned((void**)&s->h_dec, slots * 4);
   pinned((void**)&s->h_base, (size_t)m->cfg.max_batch * 8);
   pinned((void**)&s->h_cdf, (size_t)cp.m_max * ((size_t)m->cfg.vocab + 1) * 4);
+  pinned((void**)&s->h_state, (size_t)m->cfg.max_batch * m->cfg.max_chunk * 4);
+  pinned((void**)&s->h_rows, slots * 4);
+  pinned((void**)&s->h_selpos, slots * 4);
+  pinned((void**)&s->h_selrow, slots * 4);
+  pinned((void**)&s->h_nsel_up, ((size_t)m->cfg.max_batch + 1) * 4);
+  if (cp.schedule != DLMC_SCHED_ENTROPY) {
+    // every block of the full-length and of the final chunk must fit one pass's capacity
+    int big = 0;
+    for (int len : {s->n_full ? cp.chunk_len : 0, s->last_len})
+      for (int u : block_sizes(cp, len - std::min(cp.context, len))) big = std::max(big, u);
+    DLMC_CHECK(big <= cp.m_max, DLMC_E_INVAL,
+               "a block of the schedule exceeds m_max (" + std::to_string(big) + ")");
+  }
   DLMC_HIP(hipMemsetAsync(m->err, 0, 4, m->stream));
 }
 
@@ -347,6 +541,15 @@ void parse_header(const uint8_t* in, uint64_t len, dlmc_codec_params* cp, uint64
   cp->m_max = get<int32_t>(in, 64);
   cp->tau_bits = get<float>(in, 68);
   cp->batch = get<int32_t>(in, 72);
+  cp->schedule = get<int32_t>(in, 76);
+  cp->blocks = get<int32_t>(in, 80);
+  cp->u1 = get<int32_t>(in, 84);
+  cp->growth = get<double>(in, 88);
+  cp->coder = get<int32_t>(in, 96);
+  cp->context = get<int32_t>(in, 100);
+  cp->context_kind = get<int32_t>(in, 104);
+  cp->reserved = 0;
+  cp->context_seed = 0;  // positions are stored with each chunk
   DLMC_CHECK(cp->chunk_len >= 1, DLMC_E_FORMAT, "bad chunk length");
   DLMC_CHECK(*n_chunks == (*n + cp->chunk_len - 1) / cp->chunk_len, DLMC_E_FORMAT, "bad chunk count");
   const bool crc_on = cp->flags & DLMC_FLAG_CRC;
@@ -386,7 +589,13 @@ uint64_t encode_bound(const dlmc_codec_params& cp, uint64_t n) {
   uint64_t total = FIXED_HEADER + (nc + 1) * 8 + ((cp.flags & DLMC_FLAG_CRC) ? nc * 4 : 0);
   for (uint64_t c = 0; c < nc; ++c) {
     const uint64_t len = std::min<uint64_t>(cp.chunk_len, n - c * cp.chunk_len);
-    total += (len * (cp.cdf_bits + 1) + 7) / 8 + cp.coder_bits / 8 + 2;
+    const uint64_t ctx = std::min<uint64_t>((uint64_t)cp.context, len);
+    const uint64_t coded = len - ctx;
+    total += 6 * ctx;
+    if (cp.coder == DLMC_CODER_RANS)  // at most P + 1 bits a symbol for P <= 30, one word for P = 31
+      total += 8 + 4 * (cp.cdf_bits <= 30 ? (coded * (cp.cdf_bits + 1) + 31) / 32 : coded);
+    else
+      total += (coded * (cp.cdf_bits + 1) + 7) / 8 + cp.coder_bits / 8 + 2;
   }
   return total;
 }

@@ -26,10 +26,10 @@ def shape(**kw):
     return wl.ModelShape(**base)
 
 
-def codec(chunk, k=None, tau=float("-inf"), mmin=None, mmax=None, P=16, W=32, batch=1):
+def codec(chunk, k=None, tau=float("-inf"), mmin=None, mmax=None, P=16, W=32, batch=1, **kw):
     if k is not None:
         mmin = mmax = k
-    return wl.CodecParams(chunk, tau, mmin, mmax, P, W, batch)
+    return wl.CodecParams(chunk, tau, mmin, mmax, P, W, batch, **kw)
 
 
 def rel_err_rows(gpu, ref):
@@ -39,9 +39,13 @@ def rel_err_rows(gpu, ref):
     return float((num / den).max())
 
 
+FIXED_HEADER = 112  # container version 2
+
+
 def payloads(container: bytes):
     """Per-chunk payloads of a dlmc container (layout of include/dlmc.h)."""
     hdr = int.from_bytes(container[8:12], "little")
     nc = int.from_bytes(container[40:48], "little")
-    offs = [int.from_bytes(container[80 + 8 * c: 88 + 8 * c], "little") for c in range(nc + 1)]
+    offs = [int.from_bytes(container[FIXED_HEADER + 8 * c: FIXED_HEADER + 8 + 8 * c], "little")
+            for c in range(nc + 1)]
     return [container[hdr + offs[c]: hdr + offs[c + 1]] for c in range(nc)]

@@ -122,3 +122,31 @@ def test_logits_long_chunk_attention():
     err = rel_err_rows(lg, ref)
     log("max rel err", err)
     assert err <= 2e-2
+
+
+def test_roundtrip_8b_uniform_blocks_rans_context():
+    """The paper's best trade-off family at the 8B shape: uniform blocks of 16
+    (K = 128 on a 2048-token chunk), rANS, two random context symbols."""
+    w = wl.WORKLOADS["8b"]
+    cd = dataclasses.replace(w.codec, schedule="uniform", blocks=128, m_min=1, m_max=160,
+                             coder="rans", context=2, context_kind="random", context_seed=1)
+    toks = wl.make_tokens(w, cd.chunk_len)
+    log("round trip 8b uniform/rANS/context", cd)
+    sizes = []
+
+    def tr(d, chunk, pas, pos, ent, h):
+        if d == 0:
+            sizes.append(len(pos))
+
+    with dl.Model(w.model, max_chunk=cd.chunk_len, max_batch=1) as m:
+        m.set_trace(tr)
+        t0 = time.time()
+        data = m.encode(toks, cd)
+        t1 = time.time()
+        m.set_trace(None)
+        back = m.decode(data)
+        t2 = time.time()
+    assert np.array_equal(back, toks)
+    # 2046 masked positions in 128 blocks: 127 of 15, the last 15 + 141
+    assert sizes == [15] * 127 + [15 + 2046 - 15 * 128]
+    log(f"8b uniform: {len(data)} bytes, encode {t1 - t0:.1f}s decode {t2 - t1:.1f}s")

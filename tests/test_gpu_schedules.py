@@ -1,0 +1,98 @@
+"""GPU parity of the left-to-right block schedules (uniform block,
+progressive), the rANS coder and the initial context, through the C ABI.
+
+Block schedules fix their positions in advance, so the GPU and the oracle
+follow the same trajectory: selections and stored contexts are compared
+exactly, code lengths within 0.5%.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+
+import workloads as wl
+from oracle import driver as OD
+from oracle import weights as OW
+
+from gpu_common import codec, log, payloads, shape
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+import paper_2608_11249_amd as dl  # noqa: E402
+
+
+TINY_CASES = [
+    dict(schedule="uniform", blocks=16, m_min=16, m_max=16),
+    dict(schedule="progressive", u1=2, growth=1.5, m_min=1, m_max=128),
+    dict(schedule="uniform", blocks=12, m_min=1, m_max=32, coder="rans", context=8,
+         context_kind="random", context_seed=5),
+    dict(m_min=4, m_max=4, coder="rans", context=3, context_kind="contiguous"),
+    dict(schedule="uniform", blocks=256, m_min=1, m_max=1, coder="rans"),   # autoregressive
+]
+
+
+@pytest.mark.parametrize("kw", TINY_CASES)
+def test_tiny_against_oracle(kw):
+    """fp32 tiny model, two 256-byte chunks: same selections and contexts as
+    the oracle, code length within 0.5%, exact round trip."""
+    w = wl.WORKLOADS["tiny"]
+    cd = dataclasses.replace(w.codec, batch=2, **kw)
+    toks = wl.make_tokens(w, 512)
+    log("tiny vs oracle", kw)
+    sel = {}
+
+    def tr(d, chunk, pas, pos, ent, h):
+        if d == 0:
+            sel[(chunk, pas)] = tuple(pos)
+
+    with dl.Model(w.model, max_chunk=256, max_batch=2) as m:
+        m.set_trace(tr)
+        data = m.encode(toks, cd)
+        m.set_trace(None)
+        assert np.array_equal(m.decode(data, batch=1), toks)
+    W = OW.Weights(w.model)
+    res = OD.encode(w.model, W, toks, cd)
+    for c, (r, gp) in enumerate(zip(res, payloads(data))):
+        ctx = min(cd.context, 256)
+        assert gp[: 6 * ctx] == r.payload[: 6 * ctx]            # stored context, bit-exact
+        if cd.schedule != "entropy":
+            assert [sel[(c, p)] for p in range(r.passes)] == [tuple(s.tolist()) for s in r.selections]
+            assert (c, r.passes) not in sel
+        g, o = len(gp) - 6 * ctx, len(r.payload) - 6 * ctx
+        assert abs(g - o) <= 0.005 * o + 12, (g, o)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(schedule="uniform", blocks=7, mmin=1, mmax=16, coder="rans", context=5,
+         context_kind="random", context_seed=3),
+    dict(schedule="progressive", u1=1, growth=1.4, mmin=1, mmax=64, context=2),
+    dict(tau=2.0, mmin=1, mmax=8, coder="rans", context=4, context_kind="random", context_seed=9),
+])
+def test_bf16_batch_invariance_and_roundtrip(kw):
+    sh = shape(ffn="swiglu", norm="rmsnorm")
+    cd = codec(64, P=24, W=64, batch=4, **kw)
+    toks = wl.markov1_tokens(64 * 5 + 23, sh.vocab, 21)
+    log("bf16 batch invariance", kw)
+    with dl.Model(sh, max_chunk=64, max_batch=4) as m:
+        a = m.encode(toks, cd, crc=True)
+        b = m.encode(toks, cd, batch=1, crc=True)
+        assert payloads(a) == payloads(b)
+        assert np.array_equal(m.decode(a, batch=3), toks)
+
+
+def test_schedule_errors():
+    sh = shape()
+    toks = wl.markov1_tokens(100, sh.vocab, 1)
+    with dl.Model(sh, max_chunk=64) as m:
+        with pytest.raises(dl.DlmcError) as e:      # a 64-symbol block exceeds m_max = 8
+            m.encode(toks, codec(64, mmin=1, mmax=8, schedule="uniform", blocks=1))
+        assert e.value.code == -1
+        cd = codec(64, mmin=1, mmax=16, schedule="uniform", blocks=8, coder="rans", context=3)
+        data = bytearray(m.encode(toks, cd))
+        hdr = int.from_bytes(data[8:12], "little")
+        data[hdr] = 0xFF                               # first context position out of range
+        data[hdr + 1] = 0xFF
+        with pytest.raises(dl.DlmcError) as e:
+            m.decode(bytes(data))
+        assert e.value.code == -5

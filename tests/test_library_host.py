@@ -91,3 +91,35 @@ def test_status_strings():
     L = dl.lib()
     for code in range(-7, 1):
         assert L.dlmc_status_string(code)
+
+
+@pytest.mark.parametrize("P,V,n", [(16, 256, 700), (24, 300, 500), (24, 5000, 40), (31, 7, 200),
+                                   (16, 256, 0), (2, 3, 50)])
+def test_host_rans_matches_oracle_bytes(P, V, n):
+    rng = np.random.default_rng(P * 11 + V)
+    cdfs, syms = random_stream(rng, n, V, P)
+    start = cdfs[np.arange(n), syms] if n else np.zeros(0, np.uint32)
+    freq = (cdfs[np.arange(n), syms + 1] - start) if n else np.zeros(0, np.uint32)
+    ours = dl.rans_encode(start, freq, P)
+    enc = ORC.RansEncoder(P)
+    for s, f in zip(start, freq):
+        enc.encode(int(s), int(f))
+    assert ours == enc.finish()
+    if n:
+        assert np.array_equal(dl.rans_decode(ours, cdfs, P), syms)
+
+
+def test_host_rans_rejects_bad_input():
+    with pytest.raises(dl.DlmcError) as e:
+        dl.rans_encode([0], [0], 16)
+    assert e.value.code == -1
+    with pytest.raises(dl.DlmcError) as e:
+        dl.rans_encode([0], [1], 32)              # P > 31
+    assert e.value.code == -1
+    cdf = np.array([[0, 1, 1 << 16]], dtype=np.uint32)
+    good = dl.rans_encode([1], [(1 << 16) - 1], 16)
+    assert dl.rans_decode(good, cdf, 16).tolist() == [1]
+    for bad in (good[:-1], b"\x00" * 8, good + b"\x00\x00\x00\x00"):
+        with pytest.raises(dl.DlmcError) as e:
+            dl.rans_decode(bad, cdf, 16)
+        assert e.value.code == -5
