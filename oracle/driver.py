@@ -13,7 +13,8 @@ every chunk has its own coder state and bitstream; a final partial chunk is
 coded at its own length.
 
 Chunk payload: the initial context (c little-endian u16 positions, ascending,
-then their c u32 symbols) followed by the coder's bytes.
+then their c u32 symbols) followed by the coder's bytes -- for the symbol
+ranking back end, the varint ranks of the coded symbols in coding order.
 """
 from __future__ import annotations
 
@@ -26,6 +27,7 @@ import numpy as np
 import workloads as wl
 
 from . import model as M
+from . import ranking as R
 from .cdf import cdf_row
 from .coder import CorruptStream, RangeDecoder, RangeEncoder, RansDecoder, RansEncoder
 from .schedule import block_sizes, entropy_bits, select
@@ -61,13 +63,37 @@ def context_positions(codec, T: int, chunk_index: int) -> np.ndarray:
     raise ValueError(codec.context_kind)
 
 
+class _RankEncoder:
+    def __init__(self):
+        self.ranks = []
+
+    def finish(self) -> bytes:
+        return R.varint_encode(self.ranks)
+
+
+class _RankDecoder:
+    def __init__(self, data: bytes):
+        self.data, self.pos = data, 0
+
+    def next_rank(self) -> int:
+        (r,), self.pos = R.varint_decode(self.data, 1, self.pos)
+        return r
+
+    def done(self) -> bool:
+        return self.pos == len(self.data)
+
+
 def _encoder(codec):
+    if codec.coder == "rank":
+        return _RankEncoder()
     if codec.coder == "rans":
         return RansEncoder(codec.cdf_bits)
     return RangeEncoder(codec.coder_bits, codec.cdf_bits)
 
 
 def _decoder(codec, data: bytes):
+    if codec.coder == "rank":
+        return _RankDecoder(data)
     if codec.coder == "rans":
         return RansDecoder(data, codec.cdf_bits)
     return RangeDecoder(data, codec.coder_bits, codec.cdf_bits)
@@ -105,8 +131,11 @@ def encode_chunk(shape, W, tokens: np.ndarray, codec, forced: Optional[list] = N
         row_of = {int(p): i for i, p in enumerate(pos)}
         for p in sel:
             row = lg[row_of[int(p)]]
-            cdf = cdf_row(row, P)
             s = int(tokens[p])
+            if codec.coder == "rank":
+                enc.ranks.append(R.rank_of(row, s))
+                continue
+            cdf = cdf_row(row, P)
             f = int(cdf[s + 1] - cdf[s])
             enc.encode(int(cdf[s]), f)
             res.ideal_bits += -math.log2(f / float(1 << P))
@@ -117,7 +146,7 @@ def encode_chunk(shape, W, tokens: np.ndarray, codec, forced: Optional[list] = N
         state[sel] = tokens[sel]
         res.passes += 1
     head = ctx.astype("<u2").tobytes() + tokens[ctx].astype("<u4").tobytes()
-    if codec.coder == "rans":
+    if codec.coder in ("rans", "rank"):
         body = enc.finish()
         res.coded_bits = 8.0 * len(body)
     else:
@@ -146,11 +175,17 @@ def decode_chunk(shape, W, payload: bytes, T: int, codec) -> np.ndarray:
         sel = _selection(codec, state, shape.mask_id, pos, H, sizes, k)
         row_of = {int(p): i for i, p in enumerate(pos)}
         for p in sel:
-            cdf = cdf_row(lg[row_of[int(p)]], P)
-            state[p] = dec.decode(cdf)
+            row = lg[row_of[int(p)]]
+            if codec.coder == "rank":
+                r = dec.next_rank()
+                if r >= shape.vocab:
+                    raise CorruptStream("rank out of range")
+                state[p] = R.symbol_at(row, r)
+            else:
+                state[p] = dec.decode(cdf_row(row, P))
         k += 1
-    if codec.coder == "rans" and not dec.done():
-        raise CorruptStream("rANS stream did not end in its initial state")
+    if codec.coder in ("rans", "rank") and not dec.done():
+        raise CorruptStream("coded stream has trailing or missing data")
     return state
 
 
@@ -167,3 +202,12 @@ def decode(shape, W, payloads: List[bytes], n: int, codec) -> np.ndarray:
     parts = [decode_chunk(shape, W, p, b - a, codec)
              for p, (a, b) in zip(payloads, chunk_bounds(n, codec.chunk_len))]
     return np.concatenate(parts) if parts else np.zeros(0, dtype=np.int64)
+
+
+def pack_payloads(payloads: List[bytes], codec) -> bytes:
+    """The container's payload section: chunk payloads concatenated, compressed
+    as one block for the symbol ranking back end."""
+    blob = b"".join(payloads)
+    if codec.coder == "rank":
+        return R.compress(blob, codec.rank_compressor, codec.rank_level)
+    return blob

@@ -78,7 +78,9 @@ class CodecParams:
                     fixed-k rule (m_min = m_max = k).
       "uniform"     item 1: ``blocks`` = K left-to-right blocks per chunk.
       "progressive" item 2: left-to-right blocks of round(u1 * growth^(k-1)).
-    coder: "range" (W = coder_bits) or "rans" (64-bit state, 32-bit words).
+    coder: "range" (W = coder_bits), "rans" (64-bit state, 32-bit words) or
+    "rank" (symbol ranking: varint ranks, the container's payloads compressed
+    with rank_compressor at rank_level).
     context / context_kind (Initial Context Strategies): c symbols per chunk
     left visible and stored in the container, the first c ("contiguous") or c
     seeded-random positions ("random", seed context_seed + chunk index).
@@ -98,6 +100,8 @@ class CodecParams:
     context: int = 0
     context_kind: str = "contiguous"
     context_seed: int = 0
+    rank_compressor: str = "none"
+    rank_level: int = 0
 
 
 def fan_in_exp(fan_in: int) -> int:
