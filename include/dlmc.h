@@ -108,9 +108,13 @@ typedef struct dlmc_codec_params {
                          symbols per chunk left visible and stored in the chunk
                          payload (min(c, chunk length) for a short chunk) */
   int32_t context_kind; /* DLMC_CONTEXT_* */
-  int32_t reserved;     /* 0 */
+  int32_t rank_compressor; /* DLMC_CODER_RANK: DLMC_RANKC_* applied to the
+                              container's payload section as one block */
   uint64_t context_seed; /* random context of chunk i: the c positions with the
                             smallest keys splitmix64(splitmix64(seed + i) + p) */
+  int32_t rank_level;    /* compressor level: zlib 0..9, lzma preset 0..9,
+                            zstd 1..22, none 0 */
+  int32_t reserved;      /* 0 */
 } dlmc_codec_params;
 
 #define DLMC_SCHED_ENTROPY 0
@@ -118,6 +122,14 @@ typedef struct dlmc_codec_params {
 #define DLMC_SCHED_PROGRESSIVE 2
 #define DLMC_CODER_RANGE 0
 #define DLMC_CODER_RANS 1
+/* symbol ranking (Definition of Symbol Ranking): the rank of every coded
+ * symbol in the list ordered by non-increasing probability (equal
+ * probabilities by token id), written as unsigned LEB128 varints */
+#define DLMC_CODER_RANK 2
+#define DLMC_RANKC_NONE 0
+#define DLMC_RANKC_ZLIB 1
+#define DLMC_RANKC_LZMA 2 /* xz container, CRC-64 check */
+#define DLMC_RANKC_ZSTD 3
 #define DLMC_CONTEXT_CONTIGUOUS 0 /* the first c positions */
 #define DLMC_CONTEXT_RANDOM 1     /* c seeded-random positions */
 
@@ -205,6 +217,14 @@ dlmc_status dlmc_entropy_cdf(dlmc_model* model, const float* logits, int32_t n_r
 dlmc_status dlmc_select(dlmc_model* model, const float* entropy_bits, const int32_t* rows,
                         int32_t n_rows, int32_t B, int32_t T, float tau_bits, int32_t m_min,
                         int32_t m_max, int32_t* sel_pos, int32_t* sel_row, int32_t* n_sel);
+/* Symbol ranking on device logits[n_rows * vocab] (Definition of Symbol
+ * Ranking; equal probabilities ordered by token id): rank[i] of sym[i] in row
+ * i, and the inverse, sym[i] of rank[i] (0 <= rank < vocab; device int32
+ * arrays of n_rows, n_rows <= 65535). */
+dlmc_status dlmc_rank_rows(dlmc_model* model, const float* logits, int32_t n_rows,
+                           const int32_t* sym, int32_t* rank);
+dlmc_status dlmc_select_rank_rows(dlmc_model* model, const float* logits, int32_t n_rows,
+                                  const int32_t* rank, int32_t* sym);
 /* Copy weight tensor `tensor_id` (ids as in dlmc_model_create) to host dst in
  * its canonical [out, in] layout: bf16 bit patterns (uint16) or fp32. */
 dlmc_status dlmc_weight_copy(dlmc_model* model, int32_t tensor_id, void* dst, uint64_t bytes);

@@ -59,11 +59,13 @@ class CodecParams(ctypes.Structure):
                 ("blocks", ctypes.c_int32), ("u1", ctypes.c_int32),
                 ("growth", ctypes.c_double), ("coder", ctypes.c_int32),
                 ("context", ctypes.c_int32), ("context_kind", ctypes.c_int32),
-                ("reserved", ctypes.c_int32), ("context_seed", ctypes.c_uint64)]
+                ("rank_compressor", ctypes.c_int32), ("context_seed", ctypes.c_uint64),
+                ("rank_level", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 SCHEDULE = {"entropy": 0, "uniform": 1, "progressive": 2}
-CODER = {"range": 0, "rans": 1}
+CODER = {"range": 0, "rans": 1, "rank": 2}
+RANK_COMPRESSOR = {"none": 0, "zlib": 1, "lzma": 2, "zstd": 3}
 CONTEXT = {"contiguous": 0, "random": 1}
 
 
@@ -96,6 +98,8 @@ _SIGS = {
     "dlmc_rc_encode": (i32, [vp, vp, u64, i32, i32, vp, u64, P(u64)]),
     "dlmc_rc_decode": (i32, [vp, u64, vp, u64, i32, i32, i32, vp]),
     "dlmc_rans_encode": (i32, [vp, vp, u64, i32, vp, u64, P(u64)]),
+    "dlmc_rank_rows": (i32, [vp, vp, i32, vp, vp]),
+    "dlmc_select_rank_rows": (i32, [vp, vp, i32, vp, vp]),
     "dlmc_rans_decode": (i32, [vp, u64, vp, u64, i32, i32, vp]),
     "dlmc_status_string": (ctypes.c_char_p, [i32]),
     "dlmc_last_error": (ctypes.c_char_p, []),
@@ -150,8 +154,9 @@ def codec_params(codec, batch: Optional[int] = None, crc: bool = False) -> Codec
                        codec.m_max, codec.cdf_bits, codec.coder_bits,
                        codec.batch if batch is None else batch, FLAG_CRC if crc else 0,
                        SCHEDULE[codec.schedule], codec.blocks, codec.u1, float(codec.growth),
-                       CODER[codec.coder], codec.context, CONTEXT[codec.context_kind], 0,
-                       codec.context_seed)
+                       CODER[codec.coder], codec.context, CONTEXT[codec.context_kind],
+                       RANK_COMPRESSOR[codec.rank_compressor], codec.context_seed,
+                       codec.rank_level, 0)
 
 
 class Encoder:
@@ -323,6 +328,26 @@ class Model:
             g, cdf = g.view(n, V), cdf.view(n, V + 1)
         return H, mx, g, cdf
 
+
+    def rank_rows(self, logits, sym):
+        """Ranks of sym[i] in device logits row i (torch tensors on cuda)."""
+        import torch
+        n = int(sym.shape[0])
+        out = torch.empty(n, dtype=torch.int32, device=logits.device)
+        self.set_stream(torch.cuda.current_stream(logits.device).cuda_stream)
+        _check(lib().dlmc_rank_rows(self.handle, _ptr(logits.contiguous()), n,
+                                    _ptr(sym.contiguous()), _ptr(out)))
+        return out
+
+    def select_rank_rows(self, logits, rank):
+        """The symbol of rank[i] in device logits row i."""
+        import torch
+        n = int(rank.shape[0])
+        out = torch.empty(n, dtype=torch.int32, device=logits.device)
+        self.set_stream(torch.cuda.current_stream(logits.device).cuda_stream)
+        _check(lib().dlmc_select_rank_rows(self.handle, _ptr(logits.contiguous()), n,
+                                           _ptr(rank.contiguous()), _ptr(out)))
+        return out
     def select(self, H, rows, B: int, T: int, tau: float, m_min: int, m_max: int):
         """Schedule on device entropies; returns (sel_pos [B, m_max], sel_row, n_sel [B])."""
         import torch

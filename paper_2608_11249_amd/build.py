@@ -16,8 +16,9 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950",
           # packed fp32 VALU forms are kept out of the generated code
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-Wno-unused-command-line-argument"]
-SOURCES = ["gemm_bf16.hip", "attention.hip", "elementwise.hip", "coding.hip",
-           "model.cpp", "session.cpp", "capi.cpp"]
+SOURCES = ["gemm_bf16.hip", "attention.hip", "elementwise.hip", "coding.hip", "ranking.hip",
+           "model.cpp", "session.cpp", "compress.cpp", "capi.cpp"]
+LIBS = ["-lz", "-ldl"]
 
 
 def _compile(src: str) -> str:
@@ -36,7 +37,7 @@ def build(verbose: bool = False) -> str:
     with cf.ThreadPoolExecutor(jobs) as ex:
         objs = list(ex.map(_compile, SOURCES))
     tmp = OUT + ".tmp"
-    cmd = [HIPCC, "-shared", "-fPIC", "--offload-arch=gfx950", "-o", tmp, *objs]
+    cmd = [HIPCC, "-shared", "-fPIC", "--offload-arch=gfx950", "-o", tmp, *objs, *LIBS]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr}")

@@ -312,6 +312,73 @@ dlmc_status dlmc_profile_read(dlmc_model* m, int32_t stage, double* ms_total, ui
   });
 }
 
+namespace {
+// one "chunk" of length 1 per row: slot i commits position 0 of row i
+struct RowSlots {
+  int32_t *sel_row = nullptr, *sel_pos = nullptr, *n_sel = nullptr, *state = nullptr;
+  int64_t* base = nullptr;
+  uint32_t* pairs = nullptr;
+  explicit RowSlots(int n, hipStream_t s) {
+    DLMC_HIP(hipMalloc((void**)&sel_row, (size_t)n * 4));
+    DLMC_HIP(hipMalloc((void**)&sel_pos, (size_t)n * 4));
+    DLMC_HIP(hipMalloc((void**)&n_sel, (size_t)n * 4));
+    DLMC_HIP(hipMalloc((void**)&state, (size_t)n * 4));
+    DLMC_HIP(hipMalloc((void**)&base, (size_t)n * 8));
+    DLMC_HIP(hipMalloc((void**)&pairs, (size_t)n * 8));
+    std::vector<int32_t> idx(n), zero(n, 0), one(n, 1);
+    std::vector<int64_t> b(n);
+    for (int i = 0; i < n; ++i) idx[i] = i, b[i] = i;
+    DLMC_HIP(hipMemcpyAsync(sel_row, idx.data(), (size_t)n * 4, hipMemcpyHostToDevice, s));
+    DLMC_HIP(hipMemcpyAsync(sel_pos, zero.data(), (size_t)n * 4, hipMemcpyHostToDevice, s));
+    DLMC_HIP(hipMemcpyAsync(n_sel, one.data(), (size_t)n * 4, hipMemcpyHostToDevice, s));
+    DLMC_HIP(hipMemcpyAsync(base, b.data(), (size_t)n * 8, hipMemcpyHostToDevice, s));
+    DLMC_HIP(hipStreamSynchronize(s));
+  }
+  ~RowSlots() {
+    (void)hipFree(sel_row);
+    (void)hipFree(sel_pos);
+    (void)hipFree(n_sel);
+    (void)hipFree(state);
+    (void)hipFree(base);
+    (void)hipFree(pairs);
+  }
+};
+}  // namespace
+
+dlmc_status dlmc_rank_rows(dlmc_model* m, const float* logits, int32_t n_rows, const int32_t* sym,
+                           int32_t* rank) {
+  return guard([&] {
+    use(m);
+    DLMC_CHECK(n_rows >= 0 && n_rows <= 65535, DLMC_E_INVAL, "n_rows must be in 0..65535");
+    if (n_rows == 0) return;
+    DLMC_CHECK(logits && sym && rank, DLMC_E_INVAL, "NULL argument");
+    hipStream_t s = m->stream;
+    RowSlots r(n_rows, s);
+    rank_symbols(s, logits, r.sel_row, r.sel_pos, r.n_sel, sym, r.base, r.state, n_rows, 1, 1,
+                 m->cfg.vocab, r.pairs);
+    DLMC_HIP(hipMemcpy2DAsync(rank, 4, r.pairs, 8, 4, n_rows, hipMemcpyDeviceToDevice, s));
+    DLMC_HIP(hipStreamSynchronize(s));
+  });
+}
+
+dlmc_status dlmc_select_rank_rows(dlmc_model* m, const float* logits, int32_t n_rows,
+                                  const int32_t* rank, int32_t* sym) {
+  return guard([&] {
+    use(m);
+    DLMC_CHECK(n_rows >= 0 && n_rows <= 65535, DLMC_E_INVAL, "n_rows must be in 0..65535");
+    if (n_rows == 0) return;
+    DLMC_CHECK(logits && sym && rank, DLMC_E_INVAL, "NULL argument");
+    hipStream_t s = m->stream;
+    RowSlots r(n_rows, s);
+    std::vector<int32_t> h(n_rows);
+    DLMC_HIP(hipMemcpy(h.data(), rank, (size_t)n_rows * 4, hipMemcpyDeviceToHost));
+    for (int32_t v : h) DLMC_CHECK(v >= 0 && v < m->cfg.vocab, DLMC_E_INVAL, "rank outside the alphabet");
+    DLMC_HIP(hipMemcpyAsync(sym, rank, (size_t)n_rows * 4, hipMemcpyDeviceToDevice, s));
+    select_by_rank(s, logits, r.sel_row, r.sel_pos, r.n_sel, sym, r.state, n_rows, 1, 1, m->cfg.vocab);
+    DLMC_HIP(hipStreamSynchronize(s));
+  });
+}
+
 dlmc_status dlmc_rc_encode(const uint32_t* start, const uint32_t* freq, uint64_t n,
                            int32_t cdf_bits, int32_t coder_bits, uint8_t* out, uint64_t cap,
                            uint64_t* out_len) {

@@ -94,5 +94,14 @@ void gather_reveal(hipStream_t st, const uint32_t* cdf, const int32_t* sel_pos,
 // decode: reveal decoded symbols
 void reveal(hipStream_t st, const int32_t* sel_pos, const int32_t* n_sel, const int32_t* dec,
             int32_t* state, int B, int T, int m_max);
+// symbol ranking: encode writes (rank, symbol) pairs to out[2 * slot], decode
+// turns the ranks in dec[slot] into symbols; both reveal the symbols in state
+void rank_symbols(hipStream_t st, const float* logits, const int32_t* sel_row,
+                  const int32_t* sel_pos, const int32_t* n_sel, const int32_t* tokens,
+                  const int64_t* slot_base, int32_t* state, int B, int T, int m_max, int V,
+                  uint32_t* out);
+void select_by_rank(hipStream_t st, const float* logits, const int32_t* sel_row,
+                    const int32_t* sel_pos, const int32_t* n_sel, int32_t* dec, int32_t* state,
+                    int B, int T, int m_max, int V);
 
 }  // namespace dlmc

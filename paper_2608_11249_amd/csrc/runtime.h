@@ -108,6 +108,11 @@ struct StageTimer {
 
 namespace dlmc {
 
+// block compression of the symbol-ranking payload section (DLMC_RANKC_*)
+bool rank_compressor_ok(int kind, int level);
+std::vector<uint8_t> compress_block(int kind, int level, const std::vector<uint8_t>& in);
+std::vector<uint8_t> decompress_block(int kind, const uint8_t* in, size_t len, size_t expect);
+
 uint64_t fnv1a64(const void* data, size_t n, uint64_t h = 0xCBF29CE484222325ull);
 uint32_t crc32(const void* data, size_t n);
 void create_model(dlmc_model* m, const dlmc_model_config& cfg, uint64_t seed, int device);
@@ -136,6 +141,10 @@ struct dlmc_session {
   std::vector<dlmc::RangeDecoder> decs;
   std::vector<dlmc::RansEncoder> rencs;
   std::vector<dlmc::RansDecoder> rdecs;
+  // symbol ranking: per slot varint streams (encode output / decode input)
+  std::vector<std::vector<uint8_t>> rk_out;
+  std::vector<const uint8_t*> rk_data;
+  std::vector<size_t> rk_len, rk_pos;
   // initial context and left-to-right block schedules
   std::vector<std::vector<int32_t>> slot_ctx_pos, slot_ctx_sym;  // per slot
   std::vector<std::vector<int32_t>> slot_order;  // masked positions, ascending

@@ -20,7 +20,7 @@ namespace {
 
 constexpr uint32_t MAGIC = 0x434D4C44u;  // "DLMC" little endian
 constexpr uint32_t VERSION = 2;
-constexpr size_t FIXED_HEADER = 112;
+constexpr size_t FIXED_HEADER = 120;
 
 template <typename T>
 void put(std::vector<uint8_t>& v, size_t off, T x) {
@@ -50,8 +50,14 @@ void validate_codec(const dlmc_model* m, const dlmc_codec_params& c) {
              "chunk_len must be in 1..max_chunk");
   DLMC_CHECK(c.m_min >= 1 && c.m_max >= c.m_min && c.m_max <= 1024, DLMC_E_INVAL,
              "need 1 <= m_min <= m_max <= 1024");
-  DLMC_CHECK(c.coder == DLMC_CODER_RANGE || c.coder == DLMC_CODER_RANS, DLMC_E_INVAL, "unknown coder");
-  if (c.coder == DLMC_CODER_RANGE) {
+  DLMC_CHECK(c.coder == DLMC_CODER_RANGE || c.coder == DLMC_CODER_RANS || c.coder == DLMC_CODER_RANK,
+             DLMC_E_INVAL, "unknown coder");
+  DLMC_CHECK(c.coder == DLMC_CODER_RANK ? rank_compressor_ok(c.rank_compressor, c.rank_level)
+                                        : (c.rank_compressor == 0 && c.rank_level == 0),
+             DLMC_E_INVAL, "bad rank compressor / level");
+  if (c.coder == DLMC_CODER_RANK) {
+    // ranks need no CDF; cdf_bits is unused
+  } else if (c.coder == DLMC_CODER_RANGE) {
     DLMC_CHECK(c.coder_bits == 32 || c.coder_bits == 64, DLMC_E_INVAL, "coder_bits must be 32 or 64");
     DLMC_CHECK(c.cdf_bits >= 2 && c.cdf_bits <= c.coder_bits - 16 && (1ll << c.cdf_bits) > m->cfg.vocab,
                DLMC_E_INVAL, "need vocab < 2^cdf_bits and cdf_bits <= coder_bits - 16");
@@ -160,7 +166,8 @@ void dlmc_session::assign(int b, uint64_t chunk) {
     cpos = context_positions(cp, T, chunk);
     csym.resize(c);
     for (int j = 0; j < c; ++j) csym[j] = tokens[(size_t)h_base[b] + cpos[j]];
-    if (rans) rencs[b].reset(P);
+    if (cp.coder == DLMC_CODER_RANK) rk_out[b].clear();
+    else if (rans) rencs[b].reset(P);
     else encs[b].reset(cp.coder_bits, P);
   } else {
     const auto& p = payload[chunk];
@@ -176,7 +183,11 @@ void dlmc_session::assign(int b, uint64_t chunk) {
     }
     const uint8_t* data = p.data() + 6 * (size_t)c;
     const size_t len = p.size() - 6 * (size_t)c;
-    if (rans) {
+    if (cp.coder == DLMC_CODER_RANK) {
+      rk_data[b] = data;
+      rk_len[b] = len;
+      rk_pos[b] = 0;
+    } else if (rans) {
       if (!rdecs[b].reset(data, len, P)) throw Error(DLMC_E_CORRUPT, "not an rANS stream");
     } else {
       decs[b].reset(data, len, cp.coder_bits, P);
@@ -231,6 +242,10 @@ void dlmc_session::begin_phase() {
   decs.assign(B, RangeDecoder());
   rencs.assign(B, RansEncoder());
   rdecs.assign(B, RansDecoder());
+  rk_out.assign(B, {});
+  rk_data.assign(B, nullptr);
+  rk_len.assign(B, 0);
+  rk_pos.assign(B, 0);
   if (cp.schedule != DLMC_SCHED_ENTROPY) blocks = block_sizes(cp, T - std::min(cp.context, T));
   const uint64_t end = phase == 0 ? n_full : n_chunks;
   for (int b = 0; b < B; ++b) {
@@ -295,16 +310,23 @@ int dlmc_session::step(uint64_t* coded) {
       entropy_rows(s, m->logits, B * T, m->n_rows, V, m->H, m->mx);
     }
   }
+  const bool rank = cp.coder == DLMC_CODER_RANK;
   const size_t cdf_rec = m->prof_recs.size();
-  {
-    // work (read the row once, write the CDF) is filled in once n_sel is known
-    StageTimer t(m, DLMC_STAGE_CDF, 0.0);
-    cdf_rows(s, m->logits, m->mx, m->sel_row, m->n_sel, B, mm, V, P, m->cdf, nullptr, m->cdf_ws);
-  }
-  if (encode) {
+  if (!rank) {
+    {
+      // work (read the row once, write the CDF) is filled in once n_sel is known
+      StageTimer t(m, DLMC_STAGE_CDF, 0.0);
+      cdf_rows(s, m->logits, m->mx, m->sel_row, m->n_sel, B, mm, V, P, m->cdf, nullptr, m->cdf_ws);
+    }
+    if (encode) {
+      StageTimer t(m, DLMC_STAGE_REVEAL, 0.0);
+      gather_reveal(s, m->cdf, m->sel_pos, m->n_sel, m->tokens_dev, m->slot_base, m->state, B, T, mm,
+                    V, m->sym);
+    }
+  } else if (encode) {
     StageTimer t(m, DLMC_STAGE_REVEAL, 0.0);
-    gather_reveal(s, m->cdf, m->sel_pos, m->n_sel, m->tokens_dev, m->slot_base, m->state, B, T, mm,
-                  V, m->sym);
+    rank_symbols(s, m->logits, m->sel_row, m->sel_pos, m->n_sel, m->tokens_dev, m->slot_base,
+                 m->state, B, T, mm, V, m->sym);
   }
   DLMC_HIP(hipMemcpyAsync(h_nsel, m->n_sel, (size_t)B * 4, hipMemcpyDeviceToHost, s));
   DLMC_HIP(hipMemcpyAsync(h_pos, m->sel_pos, (size_t)B * mm * 4, hipMemcpyDeviceToHost, s));
@@ -316,6 +338,32 @@ int dlmc_session::step(uint64_t* coded) {
     int64_t committed = 0;
     for (int b = 0; b < B; ++b) committed += h_nsel[b];
     m->prof_recs[cdf_rec].work = (double)committed * (8.0 * V + 4.0);
+  }
+  if (rank && !encode) {
+    // this pass's ranks from each slot's stream -> symbols (revealed on the GPU)
+    for (int b = 0; b < B; ++b) {
+      if (slot_chunk[b] < 0) continue;
+      for (int j = 0; j < h_nsel[b]; ++j) {
+        uint64_t v = 0;
+        int shift = 0;
+        for (;;) {
+          DLMC_CHECK(rk_pos[b] < rk_len[b] && shift <= 56, DLMC_E_CORRUPT, "rank stream ended early");
+          const uint8_t byte = rk_data[b][rk_pos[b]++];
+          v |= (uint64_t)(byte & 0x7F) << shift;
+          shift += 7;
+          if (!(byte & 0x80)) break;
+        }
+        DLMC_CHECK(v < (uint64_t)V, DLMC_E_CORRUPT, "rank outside the alphabet");
+        h_dec[b * mm + j] = (int32_t)v;
+      }
+    }
+    DLMC_HIP(hipMemcpyAsync(m->dec, h_dec, (size_t)B * mm * 4, hipMemcpyHostToDevice, s));
+    {
+      StageTimer t(m, DLMC_STAGE_REVEAL, 0.0);
+      select_by_rank(s, m->logits, m->sel_row, m->sel_pos, m->n_sel, m->dec, m->state, B, T, mm, V);
+    }
+    DLMC_HIP(hipMemcpyAsync(h_dec, m->dec, (size_t)B * mm * 4, hipMemcpyDeviceToHost, s));
+    DLMC_HIP(hipStreamSynchronize(s));
   }
 
   const size_t row_words = (size_t)V + 1;
@@ -331,16 +379,30 @@ int dlmc_session::step(uint64_t* coded) {
     if (slot_chunk[b] < 0) continue;
     const int ns = h_nsel[b];
     const uint32_t* rows_cdf = nullptr;
-    if (!encode || m->trace) {
+    if (!rank && (!encode || m->trace)) {
       DLMC_HIP(hipMemcpy(h_cdf, m->cdf + (size_t)b * mm * row_words, (size_t)ns * row_words * 4,
                          hipMemcpyDeviceToHost));
       rows_cdf = h_cdf;
     }
     const uint64_t chunk = (uint64_t)slot_chunk[b];
     const uint64_t base = chunk * (uint64_t)cp.chunk_len;
+    std::vector<int32_t> syms;  // rank mode: the pass's symbols, for the trace
     for (int j = 0; j < ns; ++j) {
       const int pos = h_pos[b * mm + j];
-      if (encode) {
+      if (rank) {
+        if (encode) {
+          uint32_t v = h_sym[2 * (b * mm + j)];
+          while (v >= 0x80) {
+            rk_out[b].push_back((uint8_t)(v | 0x80));
+            v >>= 7;
+          }
+          rk_out[b].push_back((uint8_t)v);
+          syms.push_back((int32_t)h_sym[2 * (b * mm + j) + 1]);
+        } else {
+          tokens[base + pos] = h_dec[b * mm + j];
+          syms.push_back(h_dec[b * mm + j]);
+        }
+      } else if (encode) {
         const uint32_t st = h_sym[2 * (b * mm + j)], fr = h_sym[2 * (b * mm + j) + 1];
         if (cp.coder == DLMC_CODER_RANS) rencs[b].encode(st, fr);
         else encs[b].encode(st, fr);
@@ -357,7 +419,8 @@ int dlmc_session::step(uint64_t* coded) {
       std::vector<float> hv(ns);
       for (int j = 0; j < ns; ++j)
         DLMC_HIP(hipMemcpy(&hv[j], m->H + srow[b * mm + j], 4, hipMemcpyDeviceToHost));
-      const uint64_t hsh = fnv1a64(rows_cdf, (size_t)ns * row_words * 4);
+      const uint64_t hsh = rank ? fnv1a64(syms.data(), syms.size() * 4)
+                                : fnv1a64(rows_cdf, (size_t)ns * row_words * 4);
       m->trace(m->trace_user, encode ? 0 : 1, chunk, slot_pass[b], ns, h_pos + b * mm, hv.data(), hsh);
     }
     if (coded) *coded += (uint64_t)ns;
@@ -385,7 +448,9 @@ int dlmc_session::step(uint64_t* coded) {
         const auto& cpos = slot_ctx_pos[b];
         const auto& csym = slot_ctx_sym[b];
         const size_t c = cpos.size();
-        std::vector<uint8_t> body = cp.coder == DLMC_CODER_RANS ? rencs[b].finish() : encs[b].finish();
+        std::vector<uint8_t> body = cp.coder == DLMC_CODER_RANK   ? std::move(rk_out[b])
+                                    : cp.coder == DLMC_CODER_RANS ? rencs[b].finish()
+                                                                  : encs[b].finish();
         std::vector<uint8_t> pl(6 * c + body.size());
         for (size_t j = 0; j < c; ++j) {
           put<uint16_t>(pl, 2 * j, (uint16_t)cpos[j]);
@@ -395,6 +460,8 @@ int dlmc_session::step(uint64_t* coded) {
         payload[chunk] = std::move(pl);
       } else if (cp.coder == DLMC_CODER_RANS && !rdecs[b].done()) {
         throw Error(DLMC_E_CORRUPT, "rANS stream did not end in its initial state");
+      } else if (cp.coder == DLMC_CODER_RANK && rk_pos[b] != rk_len[b]) {
+        throw Error(DLMC_E_CORRUPT, "rank stream has trailing data");
       }
       if (!encode && (cp.flags & DLMC_FLAG_CRC)) {
         const uint64_t base = chunk * (uint64_t)cp.chunk_len;
@@ -425,9 +492,12 @@ int dlmc_session::step(uint64_t* coded) {
 std::vector<uint8_t> dlmc_session::container() const {
   const bool crc_on = cp.flags & DLMC_FLAG_CRC;
   const size_t hdr = FIXED_HEADER + (n_chunks + 1) * 8 + (crc_on ? n_chunks * 4 : 0);
-  size_t total = hdr;
-  for (const auto& p : payload) total += p.size();
-  std::vector<uint8_t> out(total, 0);
+  // payload section: the chunk payloads back to back; the symbol ranking back
+  // end compresses the whole section as one block
+  std::vector<uint8_t> section;
+  for (const auto& p : payload) section.insert(section.end(), p.begin(), p.end());
+  if (cp.coder == DLMC_CODER_RANK) section = compress_block(cp.rank_compressor, cp.rank_level, section);
+  std::vector<uint8_t> out(hdr + section.size(), 0);
   put<uint32_t>(out, 0, MAGIC);
   put<uint32_t>(out, 4, VERSION);
   put<uint32_t>(out, 8, (uint32_t)hdr);
@@ -450,7 +520,9 @@ std::vector<uint8_t> dlmc_session::container() const {
   put<int32_t>(out, 96, cp.coder);
   put<int32_t>(out, 100, cp.context);
   put<int32_t>(out, 104, cp.context_kind);
-  uint64_t off = 0;
+  put<int32_t>(out, 108, cp.rank_compressor);
+  put<int32_t>(out, 112, cp.rank_level);
+  uint64_t off = 0;  // offsets into the (uncompressed) payload section
   for (uint64_t c = 0; c <= n_chunks; ++c) {
     put<uint64_t>(out, FIXED_HEADER + c * 8, off);
     if (c < n_chunks) off += payload[c].size();
@@ -462,11 +534,7 @@ std::vector<uint8_t> dlmc_session::container() const {
       put<uint32_t>(out, FIXED_HEADER + (n_chunks + 1) * 8 + c * 4,
                     crc32(&tokens[a], (size_t)(b - a) * 4));
     }
-  size_t w = hdr;
-  for (const auto& p : payload) {
-    if (!p.empty()) std::memcpy(out.data() + w, p.data(), p.size());
-    w += p.size();
-  }
+  if (!section.empty()) std::memcpy(out.data() + hdr, section.data(), section.size());
   return out;
 }
 
@@ -548,6 +616,8 @@ void parse_header(const uint8_t* in, uint64_t len, dlmc_codec_params* cp, uint64
   cp->coder = get<int32_t>(in, 96);
   cp->context = get<int32_t>(in, 100);
   cp->context_kind = get<int32_t>(in, 104);
+  cp->rank_compressor = get<int32_t>(in, 108);
+  cp->rank_level = get<int32_t>(in, 112);
   cp->reserved = 0;
   cp->context_seed = 0;  // positions are stored with each chunk
   DLMC_CHECK(cp->chunk_len >= 1, DLMC_E_FORMAT, "bad chunk length");
@@ -572,12 +642,24 @@ dlmc_session* make_decoder(dlmc_model* m, const uint8_t* in, uint64_t len, int32
   s->tokens.assign(n, 0);
   s->payload.resize(nc);
   s->crc.resize(nc);
+  const uint64_t total = get<uint64_t>(in, FIXED_HEADER + nc * 8);
+  DLMC_CHECK(get<uint64_t>(in, FIXED_HEADER) == 0, DLMC_E_FORMAT, "bad chunk offsets");
+  std::vector<uint8_t> unpacked;
+  const uint8_t* section = in + hdr;
+  if (cp.coder == DLMC_CODER_RANK) {
+    // context and varint ranks take at most 11 bytes a token
+    DLMC_CHECK(total <= 16 * n + 1024, DLMC_E_FORMAT, "bad payload size");
+    unpacked = decompress_block(cp.rank_compressor, in + hdr, len - hdr, total);
+    section = unpacked.data();
+  } else {
+    DLMC_CHECK(hdr + total <= len, DLMC_E_FORMAT, "bad chunk offsets");
+  }
   uint64_t prev = 0;
   for (uint64_t c = 0; c < nc; ++c) {
     const uint64_t a = get<uint64_t>(in, FIXED_HEADER + c * 8);
     const uint64_t b = get<uint64_t>(in, FIXED_HEADER + (c + 1) * 8);
-    DLMC_CHECK(a == prev && b >= a && hdr + b <= len, DLMC_E_FORMAT, "bad chunk offsets");
-    s->payload[c].assign(in + hdr + a, in + hdr + b);
+    DLMC_CHECK(a == prev && b >= a && b <= total, DLMC_E_FORMAT, "bad chunk offsets");
+    s->payload[c].assign(section + a, section + b);
     prev = b;
     if (cp.flags & DLMC_FLAG_CRC) s->crc[c] = get<uint32_t>(in, FIXED_HEADER + (nc + 1) * 8 + c * 4);
   }
@@ -592,10 +674,17 @@ uint64_t encode_bound(const dlmc_codec_params& cp, uint64_t n) {
     const uint64_t ctx = std::min<uint64_t>((uint64_t)cp.context, len);
     const uint64_t coded = len - ctx;
     total += 6 * ctx;
-    if (cp.coder == DLMC_CODER_RANS)  // at most P + 1 bits a symbol for P <= 30, one word for P = 31
+    if (cp.coder == DLMC_CODER_RANK)  // a rank below 2^30 takes at most 5 varint bytes
+      total += 5 * coded;
+    else if (cp.coder == DLMC_CODER_RANS)  // at most P + 1 bits a symbol for P <= 30, one word for P = 31
       total += 8 + 4 * (cp.cdf_bits <= 30 ? (coded * (cp.cdf_bits + 1) + 31) / 32 : coded);
     else
       total += (coded * (cp.cdf_bits + 1) + 7) / 8 + cp.coder_bits / 8 + 2;
+  }
+  if (cp.coder == DLMC_CODER_RANK) {
+    // room for a compressor's worst case on incompressible input
+    const uint64_t body = total - (FIXED_HEADER + (nc + 1) * 8 + ((cp.flags & DLMC_FLAG_CRC) ? nc * 4 : 0));
+    total += body / 128 + 1024;
   }
   return total;
 }

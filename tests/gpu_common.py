@@ -39,7 +39,7 @@ def rel_err_rows(gpu, ref):
     return float((num / den).max())
 
 
-FIXED_HEADER = 112  # container version 2
+FIXED_HEADER = 120  # container version 2
 
 
 def payloads(container: bytes):
