@@ -94,6 +94,37 @@ def cpu_baseline(w, layers_timed=1, vocab_sample=4096):
     }
 
 
+def roundtrip_leg(model, w):
+    """One batch of whole chunks encoded into a container, then decoded, each
+    timed end to end (host tokens in, host bytes out): decode throughput and
+    bits per input byte, which the timed encode passes cannot give."""
+    import numpy as np
+    import torch
+
+    import workloads as wl
+    cd = w.codec
+    toks = wl.make_tokens(w, cd.batch * cd.chunk_len)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    data = model.encode(toks, cd)
+    t1 = time.perf_counter()
+    back = model.decode(data)
+    t2 = time.perf_counter()
+    if not np.array_equal(back, toks):
+        raise RuntimeError("round trip mismatch")
+    nb = len(toks) * w.token_bytes
+    return {
+        "tokens": int(len(toks)),
+        "container_bytes": len(data),
+        "bits_per_input_byte": round(8.0 * len(data) / nb, 4),
+        "encode_s": round(t1 - t0, 3),
+        "decode_s": round(t2 - t1, 3),
+        "encode_bytes_per_s": round(nb / (t1 - t0), 1),
+        "decode_bytes_per_s": round(nb / (t2 - t1), 1),
+        "note": "random-init weights: the ratio exercises the coder only",
+    }
+
+
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ffn_in_gemm_8b_traffic.md")
 GEMM_SOURCE = os.path.join(ROOT, "paper_2608_11249_amd", "csrc", "gemm_bf16.hip")
 
@@ -110,8 +141,8 @@ def measured_traffic():
         return None
     vals = {}
     for line in open(TRAFFIC_FILE):
-        if ":" in line and line.startswith("- "):
-            k, v = line[2:].split(":", 1)
+        if ": " in line and line.startswith("- "):
+            k, v = line[2:].split(": ", 1)
             vals[k.strip()] = v.strip().strip("`")
     if vals.get("gemm_bf16.hip sha256[:16]") != gemm_source_hash():
         return None
@@ -143,6 +174,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-all", action="store_true",
                     help="time every stage inside the timed region (adds event overhead)")
+    ap.add_argument("--no-decode", action="store_true",
+                    help="skip the whole-chunk encode + decode leg (detail.roundtrip)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES (counter calibration)")
     args = ap.parse_args()
@@ -238,6 +271,8 @@ def main():
             "stage_ms_one_profiled_pass": stages_ms,
         },
     }
+    if not args.no_decode:
+        out["detail"]["roundtrip"] = roundtrip_leg(model, w)
     model.close()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w)
