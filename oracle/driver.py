@@ -30,6 +30,7 @@ from . import model as M
 from . import ranking as R
 from .cdf import cdf_row
 from .coder import CorruptStream, RangeDecoder, RangeEncoder, RansDecoder, RansEncoder
+from .context import attention_context
 from .schedule import block_sizes, entropy_bits, select
 
 
@@ -49,12 +50,16 @@ def _pass(shape, W, state):
     return lg, pos, entropy_bits(lg)
 
 
-def context_positions(codec, T: int, chunk_index: int) -> np.ndarray:
-    """The chunk's initial-context positions (ascending): the first c, or the c
-    positions with the smallest seeded keys (seed context_seed + chunk index)."""
+def context_positions(codec, T: int, chunk_index: int, shape=None, W=None,
+                      tokens=None) -> np.ndarray:
+    """The chunk's initial-context positions (ascending): the first c, the c
+    positions with the smallest seeded keys (seed context_seed + chunk index),
+    or the c highest attention-rollout scores (needs the model and tokens)."""
     c = min(int(codec.context), T)
     if c == 0:
         return np.zeros(0, dtype=np.int64)
+    if codec.context_kind == "attention":
+        return attention_context(shape, W, tokens, c)
     if codec.context_kind == "contiguous":
         return np.arange(c, dtype=np.int64)
     if codec.context_kind == "random":
@@ -114,7 +119,7 @@ def encode_chunk(shape, W, tokens: np.ndarray, codec, forced: Optional[list] = N
     tokens = np.asarray(tokens, dtype=np.int64)
     T = tokens.shape[0]
     state = np.full(T, shape.mask_id, dtype=np.int64)
-    ctx = context_positions(codec, T, chunk_index)
+    ctx = context_positions(codec, T, chunk_index, shape, W, tokens)
     state[ctx] = tokens[ctx]
     sizes = None if codec.schedule == "entropy" else block_sizes(codec, T - len(ctx))
     enc = _encoder(codec)

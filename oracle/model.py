@@ -60,14 +60,16 @@ def softmax(s: np.ndarray, axis: int = -1) -> np.ndarray:
     return e / e.sum(axis=axis, keepdims=True)
 
 
-def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray) -> np.ndarray:
-    """Full (non-causal) softmax attention; q, k, v are [T, H, d_head]."""
+def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, want_probs: bool = False):
+    """Full (non-causal) softmax attention; q, k, v are [T, H, d_head].  With
+    want_probs also the probabilities [H, Tq, Tk]."""
     d_head = q.shape[-1]
     qh = np.ascontiguousarray(q.transpose(1, 0, 2))      # [H, T, dh]
     kh = np.ascontiguousarray(k.transpose(1, 2, 0))      # [H, dh, T]
     vh = np.ascontiguousarray(v.transpose(1, 0, 2))      # [H, T, dh]
     p = softmax((qh @ kh) / math.sqrt(d_head), axis=-1)  # [H, Tq, Tk]
-    return (p @ vh).transpose(1, 0, 2)
+    o = (p @ vh).transpose(1, 0, 2)
+    return (o, p) if want_probs else o
 
 
 def gelu(x: np.ndarray) -> np.ndarray:
@@ -78,8 +80,10 @@ def silu(x: np.ndarray) -> np.ndarray:
     return x / (1.0 + np.exp(-x))
 
 
-def block(shape, w: dict, x: np.ndarray, cos, sin, rope: bool = True) -> np.ndarray:
-    """One pre-norm transformer block on the residual stream x [T, d]."""
+def block(shape, w: dict, x: np.ndarray, cos, sin, rope: bool = True, probs_out=None) -> np.ndarray:
+    """One pre-norm transformer block on the residual stream x [T, d].  If
+    probs_out is a list, the head-averaged attention probabilities [Tq, Tk]
+    of the block are appended to it."""
     T, d = x.shape
     H, dh = shape.n_heads, shape.d_head
     h = norm(shape, x)
@@ -88,7 +92,12 @@ def block(shape, w: dict, x: np.ndarray, cos, sin, rope: bool = True) -> np.ndar
     v = (h @ w["v"].T).reshape(T, H, dh)
     if rope:
         q, k = apply_rope(q, cos, sin), apply_rope(k, cos, sin)
-    o = attention(q, k, v).reshape(T, d)
+    if probs_out is None:
+        o = attention(q, k, v).reshape(T, d)
+    else:
+        o, p = attention(q, k, v, want_probs=True)
+        o = o.reshape(T, d)
+        probs_out.append(p.mean(axis=0))
     x = x + o @ w["o"].T
     h = norm(shape, x)
     if shape.ffn == "gelu":

@@ -82,8 +82,9 @@ class CodecParams:
     "rank" (symbol ranking: varint ranks, the container's payloads compressed
     with rank_compressor at rank_level).
     context / context_kind (Initial Context Strategies): c symbols per chunk
-    left visible and stored in the container, the first c ("contiguous") or c
-    seeded-random positions ("random", seed context_seed + chunk index).
+    left visible and stored in the container, the first c ("contiguous"), c
+    seeded-random positions ("random", seed context_seed + chunk index), or
+    the c positions with the highest attention-rollout scores ("attention").
     """
     chunk_len: int
     tau_bits: float
