@@ -132,6 +132,10 @@ typedef struct dlmc_codec_params {
 #define DLMC_RANKC_ZSTD 3
 #define DLMC_CONTEXT_CONTIGUOUS 0 /* the first c positions */
 #define DLMC_CONTEXT_RANDOM 1     /* c seeded-random positions */
+/* the c positions with the highest Attention Rollout flow into the masked
+ * positions of two extra passes (even, then odd positions masked); each
+ * position is scored in the pass where it is visible, ties by position */
+#define DLMC_CONTEXT_ATTENTION 2
 
 #define DLMC_FLAG_CRC 1 /* store and check a CRC-32 of every chunk's tokens */
 
@@ -225,6 +229,9 @@ dlmc_status dlmc_rank_rows(dlmc_model* model, const float* logits, int32_t n_row
                            const int32_t* sym, int32_t* rank);
 dlmc_status dlmc_select_rank_rows(dlmc_model* model, const float* logits, int32_t n_rows,
                                   const int32_t* rank, int32_t* sym);
+/* Attention-based context scores of one chunk of host tokens[0..T) into
+ * host scores[0..T) (two extra forward passes, T <= max_chunk). */
+dlmc_status dlmc_context_scores(dlmc_model* model, const int32_t* tokens, int32_t T, float* scores);
 /* Copy weight tensor `tensor_id` (ids as in dlmc_model_create) to host dst in
  * its canonical [out, in] layout: bf16 bit patterns (uint16) or fp32. */
 dlmc_status dlmc_weight_copy(dlmc_model* model, int32_t tensor_id, void* dst, uint64_t bytes);

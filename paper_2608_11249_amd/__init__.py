@@ -66,7 +66,7 @@ class CodecParams(ctypes.Structure):
 SCHEDULE = {"entropy": 0, "uniform": 1, "progressive": 2}
 CODER = {"range": 0, "rans": 1, "rank": 2}
 RANK_COMPRESSOR = {"none": 0, "zlib": 1, "lzma": 2, "zstd": 3}
-CONTEXT = {"contiguous": 0, "random": 1}
+CONTEXT = {"contiguous": 0, "random": 1, "attention": 2}
 
 
 TRACE_FN = ctypes.CFUNCTYPE(None, ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint64,
@@ -99,6 +99,7 @@ _SIGS = {
     "dlmc_rc_decode": (i32, [vp, u64, vp, u64, i32, i32, i32, vp]),
     "dlmc_rans_encode": (i32, [vp, vp, u64, i32, vp, u64, P(u64)]),
     "dlmc_rank_rows": (i32, [vp, vp, i32, vp, vp]),
+    "dlmc_context_scores": (i32, [vp, vp, i32, vp]),
     "dlmc_select_rank_rows": (i32, [vp, vp, i32, vp, vp]),
     "dlmc_rans_decode": (i32, [vp, u64, vp, u64, i32, i32, vp]),
     "dlmc_status_string": (ctypes.c_char_p, [i32]),
@@ -328,6 +329,13 @@ class Model:
             g, cdf = g.view(n, V), cdf.view(n, V + 1)
         return H, mx, g, cdf
 
+
+    def context_scores(self, tokens) -> np.ndarray:
+        """Attention-based context score of every position of one chunk."""
+        t = np.ascontiguousarray(tokens, dtype=np.int32)
+        out = np.empty(len(t), dtype=np.float32)
+        _check(lib().dlmc_context_scores(self.handle, _ptr(t), len(t), _ptr(out)))
+        return out
 
     def rank_rows(self, logits, sym):
         """Ranks of sym[i] in device logits row i (torch tensors on cuda)."""

@@ -16,7 +16,7 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950",
           # packed fp32 VALU forms are kept out of the generated code
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-Wno-unused-command-line-argument"]
-SOURCES = ["gemm_bf16.hip", "attention.hip", "elementwise.hip", "coding.hip", "ranking.hip",
+SOURCES = ["gemm_bf16.hip", "attention.hip", "elementwise.hip", "coding.hip", "ranking.hip", "context.hip",
            "model.cpp", "session.cpp", "compress.cpp", "capi.cpp"]
 LIBS = ["-lz", "-ldl"]
 

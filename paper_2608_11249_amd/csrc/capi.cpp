@@ -345,6 +345,19 @@ struct RowSlots {
 };
 }  // namespace
 
+dlmc_status dlmc_context_scores(dlmc_model* m, const int32_t* tokens, int32_t T, float* scores) {
+  return guard([&] {
+    use(m);
+    DLMC_CHECK(tokens && scores, DLMC_E_INVAL, "NULL argument");
+    DLMC_CHECK(T >= 1 && T <= m->cfg.max_chunk, DLMC_E_INVAL, "T must be in 1..max_chunk");
+    for (int i = 0; i < T; ++i)
+      DLMC_CHECK(tokens[i] >= 0 && tokens[i] < m->cfg.vocab, DLMC_E_INVAL, "token outside [0, vocab)");
+    std::vector<float> sc;
+    m->context_scores(tokens, T, sc);
+    std::memcpy(scores, sc.data(), (size_t)T * 4);
+  });
+}
+
 dlmc_status dlmc_rank_rows(dlmc_model* m, const float* logits, int32_t n_rows, const int32_t* sym,
                            int32_t* rank) {
   return guard([&] {

@@ -94,6 +94,11 @@ void gather_reveal(hipStream_t st, const uint32_t* cdf, const int32_t* sel_pos,
 // decode: reveal decoded symbols
 void reveal(hipStream_t st, const int32_t* sel_pos, const int32_t* n_sel, const int32_t* dec,
             int32_t* state, int B, int T, int m_max);
+// attention-based context: A[i, :] (+)= w softmax(scale S[i, :]) (rows T,
+// pitch T), and out = (A^T v + v) / 2
+void softmax_accumulate(hipStream_t st, const float* S, float* A, int T, float scale, float w,
+                        bool first);
+void rollout_step(hipStream_t st, const float* A, const float* v, float* out, int T);
 // symbol ranking: encode writes (rank, symbol) pairs to out[2 * slot], decode
 // turns the ranks in dec[slot] into symbols; both reveal the symbols in state
 void rank_symbols(hipStream_t st, const float* logits, const int32_t* sel_row,

@@ -269,7 +269,7 @@ uint64_t dlmc_model::hash() const {
 }
 
 void dlmc_model::forward(const int32_t* st_dev, int B, int T, float* logits_out, int32_t* rows_out,
-                         int32_t* n_rows_out, int64_t rows_hint, bool rows_given) {
+                         int32_t* n_rows_out, int64_t rows_hint, bool rows_given, float* attn_maps) {
   DLMC_CHECK(B >= 1 && B <= cfg.max_batch && T >= 1 && T <= cfg.max_chunk, DLMC_E_INVAL,
              "batch / chunk length exceed the model's workspace");
   const int d = cfg.d_model, F = cfg.d_ffn, V = cfg.vocab, H = cfg.n_heads;
@@ -302,6 +302,25 @@ void dlmc_model::forward(const int32_t* st_dev, int B, int T, float* logits_out,
   resid.out = x;
   resid.ldo = d;
   const double norm_bytes = Md * dd * (4.0 + es);
+  DLMC_CHECK(!attn_maps || B == 1, DLMC_E_INVAL, "attention maps are taken one chunk at a time");
+  // head-averaged attention probabilities of layer l into attn_maps[l] (one
+  // S = Q_h K_h^T product per head, softmax added in head order)
+  auto attention_map = [&](int l) {
+    float* A = attn_maps + (size_t)l * T * T;
+    const float scale = 1.0f / std::sqrt((float)dh);
+    for (int hd = 0; hd < H; ++hd) {
+      EpiArgs e;
+      e.out = ctx_S;
+      e.ldo = T;
+      const size_t off = (size_t)hd * Tp * dh;
+      if (bf16)
+        gemm_bf16(s, (const bf16_t*)q + off, (const bf16_t*)k + off, T, T, dh, nullptr, EPI_STORE_F32, e);
+      else
+        gemm_f32(s, (const float*)q + off, (const float*)k + off, T, T, dh, nullptr, EPI_STORE_F32, e);
+      softmax_accumulate(s, ctx_S, A, T, scale, 1.0f / H, hd == 0);
+    }
+  };
+  int layer_index = 0;
   for (const Layer& w : layers) {
     {
       StageTimer t(this, DLMC_STAGE_NORM, norm_bytes);
@@ -312,6 +331,7 @@ void dlmc_model::forward(const int32_t* st_dev, int B, int T, float* logits_out,
         StageTimer t(this, DLMC_STAGE_QKV, 2.0 * Md * 3.0 * dd * dd);
         gemm_bf16(s, (const bf16_t*)h, (const bf16_t*)w.wqkv, M, 3 * d, d, nullptr, EPI_QKV_ROPE, qkv);
       }
+      if (attn_maps) attention_map(layer_index);
       {
         StageTimer t(this, DLMC_STAGE_ATTN, 4.0 * B * H * (double)T * T * dh);
         attention_bf16(s, (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)vt, (bf16_t*)attn, B, H, T, Tp, dh);
@@ -329,6 +349,7 @@ void dlmc_model::forward(const int32_t* st_dev, int B, int T, float* logits_out,
         gemm_f32(s, (const float*)h, (const float*)w.wqkv, M, 3 * d, d, nullptr, EPI_STORE_F32, t3);
         qkv_rope_f32(s, tmp, M, qkv);
       }
+      if (attn_maps) attention_map(layer_index);
       {
         StageTimer t(this, DLMC_STAGE_ATTN, 4.0 * B * H * (double)T * T * dh);
         attention_f32(s, (const float*)q, (const float*)k, (const float*)vt, (float*)attn, B, H, T, Tp, dh);
@@ -369,7 +390,9 @@ void dlmc_model::forward(const int32_t* st_dev, int B, int T, float* logits_out,
         gemm_f32(s, (const float*)ffn, (const float*)w.wout, M, d, F, nullptr, EPI_RESIDUAL, resid);
       }
     }
+    ++layer_index;
   }
+  if (attn_maps) return;  // context passes need no head
   // masked (or given) rows only: compaction, final norm gathered, LM head
   if (!rows_given) {
     StageTimer t(this, DLMC_STAGE_COMPACT, Md * 8.0);
@@ -388,4 +411,43 @@ void dlmc_model::forward(const int32_t* st_dev, int B, int T, float* logits_out,
               rows_hint >= 0 ? (int)rows_hint : -1);
   else
     gemm_f32(s, (const float*)hm, (const float*)this->head, M, V, d, nr, EPI_STORE_F32, o);
+}
+
+void dlmc_model::context_scores(const int32_t* tokens, int T, std::vector<float>& score) {
+  DLMC_CHECK(T >= 1 && T <= cfg.max_chunk, DLMC_E_INVAL, "chunk length exceeds the model's workspace");
+  const int L = cfg.n_layers, V = cfg.vocab;
+  if (T > ctx_T) {
+    dfree(ctx_maps);
+    dfree(ctx_S);
+    dfree(ctx_v);
+    dfree(ctx_state);
+    ctx_maps = (float*)dalloc((size_t)std::max(L, 1) * T * T * 4);
+    ctx_S = (float*)dalloc((size_t)T * T * 4);
+    ctx_v = (float*)dalloc((size_t)2 * T * 4);
+    ctx_state = (int32_t*)dalloc((size_t)T * 4);
+    ctx_T = T;
+  }
+  score.assign(T, 0.0f);
+  std::vector<int32_t> st(T);
+  std::vector<float> v(T);
+  for (int parity = 0; parity < 2; ++parity) {
+    for (int p = 0; p < T; ++p) {
+      const bool masked = (p & 1) == parity;
+      st[p] = masked ? V : tokens[p];
+      v[p] = masked ? 1.0f : 0.0f;
+    }
+    DLMC_HIP(hipMemcpyAsync(ctx_state, st.data(), (size_t)T * 4, hipMemcpyHostToDevice, stream));
+    DLMC_HIP(hipMemcpyAsync(ctx_v, v.data(), (size_t)T * 4, hipMemcpyHostToDevice, stream));
+    forward(ctx_state, 1, T, nullptr, nullptr, nullptr, -1, false, ctx_maps);
+    // 1_M^T A~_L ... A~_1, last layer first
+    float *in = ctx_v, *out = ctx_v + T;
+    for (int l = L - 1; l >= 0; --l) {
+      rollout_step(stream, ctx_maps + (size_t)l * T * T, in, out, T);
+      std::swap(in, out);
+    }
+    DLMC_HIP(hipMemcpyAsync(v.data(), in, (size_t)T * 4, hipMemcpyDeviceToHost, stream));
+    DLMC_HIP(hipStreamSynchronize(stream));
+    for (int p = 0; p < T; ++p)
+      if ((p & 1) != parity) score[p] = v[p];
+  }
 }

@@ -81,7 +81,16 @@ struct dlmc_model {
   // rows_given the head rows are the ones already in rows / n_rows (the
   // committed rows of a block schedule) instead of the masked rows.
   void forward(const int32_t* state, int B, int T, float* logits_out, int32_t* rows_out,
-               int32_t* n_rows_out, int64_t rows_hint = -1, bool rows_given = false);
+               int32_t* n_rows_out, int64_t rows_hint = -1, bool rows_given = false,
+               float* attn_maps = nullptr);
+  // attention-based context: per layer head-averaged attention maps of one
+  // chunk (B = 1) written to attn_maps [L, T, T] by forward (the head is then
+  // skipped); context_scores runs the two half-masked passes and returns the
+  // rollout score of every position (host tokens and scores)
+  float *ctx_maps = nullptr, *ctx_S = nullptr, *ctx_v = nullptr;
+  int32_t* ctx_state = nullptr;
+  int ctx_T = 0;
+  void context_scores(const int32_t* tokens, int T, std::vector<float>& score);
 };
 
 namespace dlmc {

@@ -73,7 +73,7 @@ void validate_codec(const dlmc_model* m, const dlmc_codec_params& c) {
                  (c.u1 >= 1 && std::isfinite(c.growth) && c.growth > 0.0),
              DLMC_E_INVAL, "progressive schedule needs u1 >= 1 and a finite growth > 0");
   DLMC_CHECK(c.context >= 0 && c.context <= 8192, DLMC_E_INVAL, "context must be in 0..8192");
-  DLMC_CHECK(c.context_kind == DLMC_CONTEXT_CONTIGUOUS || c.context_kind == DLMC_CONTEXT_RANDOM,
+  DLMC_CHECK(c.context_kind >= DLMC_CONTEXT_CONTIGUOUS && c.context_kind <= DLMC_CONTEXT_ATTENTION,
              DLMC_E_INVAL, "unknown context kind");
   DLMC_CHECK(c.reserved == 0, DLMC_E_INVAL, "reserved field must be 0");
   DLMC_CHECK(c.batch >= 1 && c.batch <= m->cfg.max_batch, DLMC_E_INVAL, "batch must be in 1..max_batch");
@@ -163,7 +163,18 @@ void dlmc_session::assign(int b, uint64_t chunk) {
   auto& cpos = slot_ctx_pos[b];
   auto& csym = slot_ctx_sym[b];
   if (encode) {
-    cpos = context_positions(cp, T, chunk);
+    if (cp.context_kind == DLMC_CONTEXT_ATTENTION && c > 0) {
+      // two extra passes over this chunk; the c highest scores, ties by position
+      std::vector<float> sc;
+      m->context_scores(tokens.data() + h_base[b], T, sc);
+      std::vector<int32_t> ord(T);
+      for (int p = 0; p < T; ++p) ord[p] = p;
+      std::stable_sort(ord.begin(), ord.end(), [&](int x, int y) { return sc[x] > sc[y]; });
+      cpos.assign(ord.begin(), ord.begin() + c);
+      std::sort(cpos.begin(), cpos.end());
+    } else {
+      cpos = context_positions(cp, T, chunk);
+    }
     csym.resize(c);
     for (int j = 0; j < c; ++j) csym[j] = tokens[(size_t)h_base[b] + cpos[j]];
     if (cp.coder == DLMC_CODER_RANK) rk_out[b].clear();

@@ -150,3 +150,25 @@ def test_roundtrip_8b_uniform_blocks_rans_context():
     # 2046 masked positions in 128 blocks: 127 of 15, the last 15 + 141
     assert sizes == [15] * 127 + [15 + 2046 - 15 * 128]
     log(f"8b uniform: {len(data)} bytes, encode {t1 - t0:.1f}s decode {t2 - t1:.1f}s")
+
+
+def test_roundtrip_8b_attention_context():
+    """Attention-based context at the 8B shape: two extra passes store and read
+    32 head-averaged 2048 x 2048 maps; the stored context is the top of the
+    GPU's own scores."""
+    w = wl.WORKLOADS["8b"]
+    cd = dataclasses.replace(w.codec, schedule="uniform", blocks=128, m_min=1, m_max=160,
+                             coder="rans", context=8, context_kind="attention")
+    toks = wl.make_tokens(w, cd.chunk_len)
+    log("round trip 8b attention context", cd)
+    with dl.Model(w.model, max_chunk=cd.chunk_len, max_batch=1) as m:
+        t0 = time.time()
+        data = m.encode(toks, cd)
+        t1 = time.time()
+        back = m.decode(data)
+        sc = m.context_scores(toks)
+    assert np.array_equal(back, toks)
+    top = sorted(sorted(range(len(toks)), key=lambda j: (-sc[j], j))[:8])
+    (p,) = payloads(data)
+    assert np.frombuffer(p[:16], dtype="<u2").tolist() == top
+    log(f"8b attention context: encode {t1 - t0:.1f}s, context {top}")

@@ -96,3 +96,43 @@ def test_schedule_errors():
         with pytest.raises(dl.DlmcError) as e:
             m.decode(bytes(data))
         assert e.value.code == -5
+
+
+# ---------------------------------------------------------------- attention-based context
+from oracle import context as OX  # noqa: E402
+
+
+@pytest.mark.parametrize("T", [64, 256])
+def test_context_scores_against_oracle_fp32(T):
+    w = wl.WORKLOADS["tiny"]
+    toks = wl.make_tokens(w, T)
+    log("context scores fp32", T)
+    with dl.Model(w.model, max_chunk=T) as m:
+        got = m.context_scores(toks).astype(np.float64)
+    ref = OX.context_scores(w.model, OW.Weights(w.model), toks)
+    assert np.max(np.abs(got - ref)) <= 1e-4 * np.max(np.abs(ref)) + 1e-6
+    # the selection wherever the c-th boundary is clear of the numeric error
+    order = sorted(range(T), key=lambda j: (-ref[j], j))
+    for c in (1, 5, T // 4):
+        if ref[order[c - 1]] - ref[order[c]] > 1e-3 * np.max(np.abs(ref)):
+            sel = sorted(range(T), key=lambda j: (-got[j], j))[:c]
+            assert sorted(sel) == sorted(order[:c]), c
+
+
+def test_attention_context_roundtrip_and_stored_positions_bf16():
+    sh = shape(ffn="swiglu", norm="rmsnorm")
+    cd = codec(64, P=24, W=64, batch=2, mmin=4, mmax=4, coder="rans", context=6,
+               context_kind="attention")
+    toks = wl.markov1_tokens(64 * 2 + 20, sh.vocab, 31)
+    log("attention context bf16")
+    with dl.Model(sh, max_chunk=64, max_batch=2) as m:
+        data = m.encode(toks, cd)
+        assert np.array_equal(m.decode(data, batch=1), toks)
+        for c, p in enumerate(payloads(data)):
+            seg = toks[64 * c: 64 * (c + 1)]
+            sc = m.context_scores(seg)
+            top = sorted(sorted(range(len(seg)), key=lambda j: (-sc[j], j))[:min(6, len(seg))])
+            assert np.frombuffer(p[: 2 * len(top)], dtype="<u2").tolist() == top
+        ref = OX.context_scores(sh, OW.Weights(sh), toks[:64])
+        got = m.context_scores(toks[:64]).astype(np.float64)
+    assert np.max(np.abs(got - ref)) <= 3e-2 * np.max(np.abs(ref))
