@@ -19,12 +19,16 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950",
 SOURCES = ["gemm_bf16.hip", "attention.hip", "elementwise.hip", "coding.hip", "ranking.hip", "context.hip",
            "model.cpp", "session.cpp", "compress.cpp", "capi.cpp"]
 LIBS = ["-lz", "-ldl"]
+# per-source flags: attention produces no NaN from finite inputs, so max()
+# needs no NaN canonicalisation of the MFMA results (infinities keep their
+# meaning: masked keys are -inf)
+EXTRA = {"attention.hip": ["-fno-honor-nans"]}
 
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, src.rsplit(".", 1)[0] + ".o")
     lang = ["-x", "hip"] if src.endswith(".hip") else []
-    cmd = [HIPCC, *COMMON, *lang, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *COMMON, *EXTRA.get(src, []), *lang, "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"compile of {src} failed:\n{r.stderr}")

@@ -17,6 +17,8 @@
 // registers stage them and two waves fit per SIMD.  Key tiles are visited in
 // a fixed order, so results do not depend on the launch shape or on other
 // chunks.
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace dlmc {
@@ -103,31 +105,51 @@ attn_bf16_kernel(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kg,
       lds_dma16(Vp + kt * KT + v_src[w], &Vs[buf][(wave * VW + w) * 512]);
   };
 
+  // LDS byte offsets of this lane's fragment reads inside one K / V^T tile
+  // (loop invariant; the buffer half is a constant added per unrolled trip)
+  int koff[NS][2], voff[NV];
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    const int dc = 2 * s + lg;
+    koff[s][0] = (lr * DH + ((dc ^ kswz<DH>(lr)) << 3)) * 2;
+    koff[s][1] = ((32 + lr) * DH + ((dc ^ kswz<DH>(32 + lr)) << 3)) * 2;
+  }
+#pragma unroll
+  for (int idx = 0; idx < NV; ++idx) {
+    const int t = idx >> 2, j = idx & 3, d = t * 32 + lr, c = 2 * j + lg;
+    voff[idx] = (d * KT + ((c ^ vswz(d)) << 3)) * 2;
+  }
+
   f32x16 o[DH / 32];
 #pragma unroll
   for (int t = 0; t < DH / 32; ++t)
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[t][r] = 0.0f;
+  // Running max in log2 units.  It is raised only when a tile's max exceeds
+  // it by more than RESCALE_LOG2: until then every probability 2^(s - m_run)
+  // stays below 2^RESCALE_LOG2 (exact in fp32, no loss in bf16), and O and l
+  // share the stale max, so O / l is unchanged -- the rescale of O is skipped
+  // on most tiles.
+  constexpr float RESCALE_LOG2 = 8.0f;
   float m_run = -INFINITY, l_run = 0.0f;
 
   const int n_kt = (T + KT - 1) / KT;
-  load_tile(0, 0);
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-  for (int kt = 0; kt < n_kt; ++kt) {
-    const int cur = kt & 1, k0 = kt * KT;
+  const char* ks_base = reinterpret_cast<const char*>(&Ks[0][0]);
+  const char* vs_base = reinterpret_cast<const char*>(&Vs[0][0]);
+  auto tile = [&](int kt, auto cur_c) {
+    constexpr int cur = decltype(cur_c)::value;
+    const int k0 = kt * KT;
     if (kt + 1 < n_kt) load_tile(kt + 1, cur ^ 1);
 
     // S^T for LDS rows 0-31 (s0) and 32-63 (s1); fragments two k steps ahead
     f32x16 s0, s1;
 #pragma unroll
     for (int r = 0; r < 16; ++r) s0[r] = s1[r] = 0.0f;
-    const bf16_t* kb = Ks[cur];
+    const char* kb = ks_base + cur * KT * DH * 2;
     bf16x8 kf[3][2];
     auto kload = [&](int s, bf16x8(&f)[2]) {
-      const int dc = 2 * s + lg;
-      f[0] = *reinterpret_cast<const bf16x8*>(kb + lr * DH + ((dc ^ kswz<DH>(lr)) << 3));
-      f[1] = *reinterpret_cast<const bf16x8*>(kb + (32 + lr) * DH + ((dc ^ kswz<DH>(32 + lr)) << 3));
+      f[0] = *reinterpret_cast<const bf16x8*>(kb + koff[s][0]);
+      f[1] = *reinterpret_cast<const bf16x8*>(kb + koff[s][1]);
     };
     kload(0, kf[0]);
     kload(1, kf[1]);
@@ -148,25 +170,34 @@ attn_bf16_kernel(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kg,
         if (key + 32 >= T) s1[r] = -INFINITY;
       }
     }
-    float mx = -INFINITY;
+    float m4[4];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
+    for (int a = 0; a < 4; ++a) {
+      float m = fmaxf(s0[4 * a], s1[4 * a]);
+#pragma unroll
+      for (int e = 1; e < 4; ++e) m = fmaxf(m, fmaxf(s0[4 * a + e], s1[4 * a + e]));
+      m4[a] = m;
+    }
+    float mx = fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3]));
     mx = fmaxf(mx, __shfl_xor(mx, 32)) * scale_log2;
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = fast_exp2(m_run - m_new);
-    l_run *= alpha;
+    if (__builtin_amdgcn_ballot_w64(mx > m_run + RESCALE_LOG2)) {
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = fast_exp2(m_run - m_new);
+      l_run *= alpha;
 #pragma unroll
-    for (int t = 0; t < DH / 32; ++t)
+      for (int t = 0; t < DH / 32; ++t)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) o[t][r] *= alpha;
-    m_run = m_new;
-    float psum = 0.0f;
+        for (int r = 0; r < 16; ++r) o[t][r] *= alpha;
+      m_run = m_new;
+    }
+    float ps[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      s0[r] = fast_exp2(fmaf(s0[r], scale_log2, -m_new));
-      s1[r] = fast_exp2(fmaf(s1[r], scale_log2, -m_new));
-      psum += s0[r] + s1[r];
+      s0[r] = fast_exp2(fmaf(s0[r], scale_log2, -m_run));
+      s1[r] = fast_exp2(fmaf(s1[r], scale_log2, -m_run));
+      ps[r & 3] += s0[r] + s1[r];
     }
+    float psum = (ps[0] + ps[1]) + (ps[2] + ps[3]);
     psum += __shfl_xor(psum, 32);
     l_run += psum;
 
@@ -181,12 +212,9 @@ attn_bf16_kernel(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kg,
       pf[3][e] = (__bf16)s1[8 + e];
     }
     // O^T += V^T P^T; the V^T fragment of row d, k step j is chunk 2 j + lg
-    const bf16_t* vb = Vs[cur];
+    const char* vb = vs_base + cur * DH * KT * 2;
     bf16x8 vf[3];
-    auto vload = [&](int idx, bf16x8& f) {
-      const int t = idx >> 2, j = idx & 3, d = t * 32 + lr, c = 2 * j + lg;
-      f = *reinterpret_cast<const bf16x8*>(vb + d * KT + ((c ^ vswz(d)) << 3));
-    };
+    auto vload = [&](int idx, bf16x8& f) { f = *reinterpret_cast<const bf16x8*>(vb + voff[idx]); };
     vload(0, vf[0]);
     vload(1, vf[1]);
 #pragma unroll
@@ -197,6 +225,15 @@ attn_bf16_kernel(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kg,
     // the next tile has landed (own loads) and every wave is done with this one
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
+  };
+
+  load_tile(0, 0);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  // two tiles per trip, so each trip's buffer offsets are constants
+  for (int kt = 0; kt < n_kt; kt += 2) {
+    tile(kt, std::integral_constant<int, 0>{});
+    if (kt + 1 < n_kt) tile(kt + 1, std::integral_constant<int, 1>{});
   }
 
   const int q = q0 + lr;
