@@ -1,22 +1,21 @@
 // bf16 MFMA GEMM for gfx950 with fused epilogues: C = A * B^T, fp32 accumulate.
 //
 // Every dense contraction of the forward pass (QKV, O, FFN in/out, LM head)
-// runs here.  Block tile BM x BN x 64 with four 64-wide waves in a 2 x 2
-// grid; each wave owns a (BM/2) x (BN/2) sub-tile built from
-// v_mfma_f32_32x32x16_bf16 tiles.  Operand tiles move global -> LDS with
-// direct loads (global_load_lds_dwordx4) into a double-buffered LDS tile, one
-// barrier per k-tile.  LDS rows are 64 bf16 (128 B) with the eight 16-byte
-// chunks XOR-swizzled (swz below) so fragment loads are free of bank conflicts.  The fragment reads of k step
-// s + 1 are scheduled between the MFMAs of step s.
-//
-// Measured on MI355X (M = 2048): the fill of LDS from L2 (about 44 B/clk/CU at
-// best, latency-bound per CU) limits these shapes; two waves per SIMD (the
-// 8-wave variant) hide it best for the forward GEMMs, and the 4-wave
-// 256 x 256 tile is best for the LM head.
+// runs here.  Block tile BM x BN x 64 built from v_mfma_f32_32x32x16_bf16
+// tiles.  Operand tiles move global -> LDS with direct loads
+// (global_load_lds_dwordx4) into a double-buffered LDS tile.  LDS rows are 64
+// bf16 (128 B) with the eight 16-byte chunks XOR-swizzled (swz below) so
+// fragment loads are free of bank conflicts.  Two kernels:
+//  - gemm_bf16_kernel: four waves in a 2 x 2 grid, one barrier per k-tile,
+//    the fragment reads of k step s + 1 scheduled between the MFMAs of step s
+//    (128 x 128 tiles, two blocks per CU, and the 256 x 256 LM head);
+//  - gemm_bf16_pp_kernel: eight waves on a 256 x 256 tile in two groups that
+//    alternate memory and compute phases (the SwiGLU FFN-in GEMM).
 //
 // Numerics: each output element is a sequential sum over k-tiles, each k-tile
-// four MFMA steps in order, independent of the tile shape and of which other
-// rows are in the launch, so results are identical for any batch composition.
+// four MFMA steps in order, independent of the kernel, the tile shape and of
+// which other rows are in the launch, so results are identical for any batch
+// composition.
 #include "kernels.h"
 
 namespace dlmc {
@@ -484,19 +483,66 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, in
     epilogue<BM, BN, EPI>(acc, m0, n0, wm, wn, lane, Mv, N, ea);
 }
 
-// 8-wave variant (2 x 4 waves, two per SIMD): wave tile (BM/2) x (BN/4).
-template <int BM, int BN, int EPI>
+// ---------------------------------------------------------------------------
+// 8-wave 256 x 256 kernel with a ping-pong schedule.
+//
+// The two waves of a SIMD belong to different groups (waves 0-3 and 4-7)
+// that run one phase apart.  Per k-tile each group has a memory phase (all 24
+// MFMA fragments of the wave's 128 x 64 sub-tile read from LDS into
+// registers; group 0 also issues the direct loads of the next k-tile) and a
+// compute phase (the wave's 32 MFMAs back to back from registers, at raised
+// wave priority).  Every phase ends at a workgroup barrier, so on each SIMD
+// one wave computes while the other loads, and the MFMA pipe is fed from
+// registers instead of waiting on LDS reads, load completion and barriers.
+//
+// LDS stages: tile k sits in stage k % 2.  Group 0 issues tile k + 1 at the
+// start of its memory phase for tile k and waits for it at the end of its
+// compute phase; both groups finish reading tile k (their memory phases,
+// which end with every LDS read landed) before group 0 starts tile k + 2.
+//
+// Numerics: each accumulator takes the k steps of each k-tile in order, as in
+// gemm_bf16_kernel, so the results are identical to the other kernels'.
+__device__ __forceinline__ void pp_barrier() {
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// Direct loads of one k-tile by a group-0 wave: 8 windows of A rows and 8 of
+// B rows (rows 64 q .. 64 q + 63 of each tile).  Window j covers rows 8 j ..
+// 8 j + 7 of the wave's range; its chunk swizzle depends only on j % 2, so
+// two per-lane offsets (off[0], off[1]) serve all windows.  A tile that runs
+// past the live rows (Mv) takes clamped row indices instead.
+template <int NWIN>
+__device__ __forceinline__ void pp_issue(const bf16_t* __restrict__ src, const int (&off)[2],
+                                         size_t row_stride8, bf16_t* lds) {
+#pragma unroll
+  for (int j = 0; j < NWIN; ++j) lds_dma16(src + j * row_stride8 + off[j & 1], lds + j * 512);
+}
+template <int NWIN>
+__device__ __forceinline__ void pp_issue_clamped(const bf16_t* __restrict__ A, int first_row,
+                                                 int last_row, int K, int col, int lrow, int lane,
+                                                 bf16_t* lds) {
+#pragma unroll
+  for (int j = 0; j < NWIN; ++j) {
+    const int chunk = ((lane & 7) ^ swz(lrow + 8 * (j & 1))) << 3;
+    lds_dma16(A + (min(first_row + 8 * j, last_row) * K + col + chunk), lds + j * 512);
+  }
+}
+
+template <int EPI>
 __global__ void __launch_bounds__(512)
-gemm_bf16_w8_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, int M, int N,
-                 int K, const int* __restrict__ M_dev, EpiArgs ea, int n_tm, int n_tn) {
-  constexpr int WM = BM / 2, WN = BN / 4;  // 8 waves: 2 x 4
-  constexpr int TM = WM / 32, TN = WN / 32;
-  constexpr int A_IN = BM / 64;  // 1 KB load instructions per wave per k-tile
-  constexpr int B_IN = BN / 64;
+gemm_bf16_pp_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, int M, int N,
+                    int K, const int* __restrict__ M_dev, EpiArgs ea, int n_tm, int n_tn) {
+  constexpr int BM = 256, BN = 256, WM = 128, WN = 64, TM = WM / 32, TN = WN / 32;
+  constexpr int A_IN = BM / 32, B_IN = BN / 32;  // 1 KB direct loads per group-0 wave per k-tile
   __shared__ __attribute__((aligned(16))) bf16_t smem[StagedEpi<BM, BN, EPI>::smem_elems];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 2, wn = wave & 3;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, kept scalar
+  const int grp = wave >> 2, q = wave & 3;  // wave q of group grp owns rows 128 grp, columns 64 q
   const int lr = lane & 31, lg = lane >> 5;
   const int Mv = M_dev ? min(*M_dev, M) : M;
   int tm, tn;
@@ -506,18 +552,26 @@ gemm_bf16_w8_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw,
 
   bf16_t* As = smem;
   bf16_t* Bs = smem + 2 * BM * BK;
-  int a_off[A_IN], b_off[B_IN];
+  // group-0 direct loads: lane l of window j fills row 64 q + 8 j + l / 8,
+  // 16-byte slot l % 8, with chunk (l % 8) ^ swz(row) of that row
+  const int lrow = 64 * q + (lane >> 3);
+  int off[2];
 #pragma unroll
-  for (int j = 0; j < A_IN; ++j) {
-    const int sl = (wave * A_IN + j) * 64 + lane, row = sl >> 3;
-    a_off[j] = min(m0 + row, Mv - 1) * K + (((sl & 7) ^ swz(row)) << 3);
-  }
-#pragma unroll
-  for (int j = 0; j < B_IN; ++j) {
-    const int sl = (wave * B_IN + j) * 64 + lane, row = sl >> 3;
-    b_off[j] = min(n0 + row, N - 1) * K + (((sl & 7) ^ swz(row)) << 3);
-  }
-  const int a_win = wave * A_IN * 512, b_win = wave * B_IN * 512;  // this wave's LDS windows
+  for (int e = 0; e < 2; ++e) off[e] = lrow * K + (((lane & 7) ^ swz(lrow + 8 * e)) << 3);
+  const bool a_full = m0 + BM <= Mv;  // N % 256 == 0: B tiles are always whole
+  const size_t stride8 = (size_t)8 * K;
+  const bf16_t* a_src = A + (size_t)m0 * K;
+  const bf16_t* b_src = Bw + (size_t)n0 * K;
+  const int a_win = q * A_IN * 512, b_win = q * B_IN * 512;
+  auto issue = [&](int kt, int stage) {
+    bf16_t* as = As + stage * BM * BK + a_win;
+    bf16_t* bs = Bs + stage * BN * BK + b_win;
+    if (a_full)
+      pp_issue<A_IN>(a_src + kt * BK, off, stride8, as);
+    else
+      pp_issue_clamped<A_IN>(A, m0 + lrow, Mv - 1, K, kt * BK, lrow, lane, as);
+    pp_issue<B_IN>(b_src + kt * BK, off, stride8, bs);
+  };
 
   f32x16 acc[TM][TN];
 #pragma unroll
@@ -528,77 +582,51 @@ gemm_bf16_w8_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw,
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
   const int nk = K / BK;
-#pragma unroll
-  for (int j = 0; j < A_IN; ++j)
-    lds_dma16(A + a_off[j], As + a_win + j * 512);
-#pragma unroll
-  for (int j = 0; j < B_IN; ++j)
-    lds_dma16(Bw + b_off[j], Bs + b_win + j * 512);
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-
+  if (grp == 0) {
+    issue(0, 0);
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+  }
+  pp_barrier();
+  if (grp == 1) pp_barrier();  // group 1 runs one phase behind
   for (int kt = 0; kt < nk; ++kt) {
     const int cur = kt & 1;
-    if (kt + 1 < nk) {
-      const int k1 = (kt + 1) * BK;
-      bf16_t* an = As + (cur ^ 1) * BM * BK + a_win;
-      bf16_t* bn = Bs + (cur ^ 1) * BN * BK + b_win;
-#pragma unroll
-      for (int j = 0; j < A_IN; ++j)
-        lds_dma16(A + a_off[j] + k1, an + j * 512);
-#pragma unroll
-      for (int j = 0; j < B_IN; ++j)
-        lds_dma16(Bw + b_off[j] + k1, bn + j * 512);
-    }
+    // memory phase
+    if (grp == 0 && kt + 1 < nk) issue(kt + 1, cur ^ 1);
     const bf16_t* as = As + cur * BM * BK;
     const bf16_t* bs = Bs + cur * BN * BK;
-    bf16x8 a0[TM], b0[TN], a1[TM], b1[TN];
-    load_frags<TM>(a0, as, wm * WM, lr, lg);
-    load_frags<TN>(b0, bs, wn * WN, lr, lg);
-    load_frags<TM>(a1, as, wm * WM, lr, 2 + lg);
-    load_frags<TN>(b1, bs, wn * WN, lr, 2 + lg);
-    mfma_block<TM, TN>(acc, a0, b0);
-    load_frags<TM>(a0, as, wm * WM, lr, 4 + lg);
-    load_frags<TN>(b0, bs, wn * WN, lr, 4 + lg);
-    mfma_block<TM, TN>(acc, a1, b1);
-    load_frags<TM>(a1, as, wm * WM, lr, 6 + lg);
-    load_frags<TN>(b1, bs, wn * WN, lr, 6 + lg);
-    mfma_block<TM, TN>(acc, a0, b0);
-    mfma_block<TM, TN>(acc, a1, b1);
-    {
-      // software pipeline: the DS reads of k step s+1 and the direct loads of
-      // the next k-tile are spread between the MFMAs of k step s
-      constexpr int NF = TM + TN, NM = TM * TN, NV = A_IN + B_IN;
-      __builtin_amdgcn_sched_group_barrier(0x100, NF, 0);
+    bf16x8 fa[4][TM], fb[4][TN];
 #pragma unroll
-      for (int i = 0; i < NF; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-        if (i < NV) __builtin_amdgcn_sched_group_barrier(0x020, NV / NF > 0 ? NV / NF : 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, NM / NF, 0);
-      }
-#pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2)
-#pragma unroll
-        for (int i = 0; i < NF; ++i) {
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x008, NM / NF, 0);
-        }
-      __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
+    for (int s = 0; s < 4; ++s) {
+      load_frags<TM>(fa[s], as, grp * WM, lr, 2 * s + lg);
+      load_frags<TN>(fb[s], bs, q * WN, lr, 2 * s + lg);
     }
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave is done with the stage
+    pp_barrier();
+    // compute phase
+    __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s][j], acc[i][j], 0, 0, 0);
+    __builtin_amdgcn_s_setprio(0);
+    if (grp == 0) __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): tile kt + 1 has landed
+    pp_barrier();
   }
+  if (grp == 0) pp_barrier();  // both groups have passed the same number of barriers
   if constexpr (StagedEpi<BM, BN, EPI>::enabled)
-    epilogue_staged<BM, BN, EPI, WM, WN, 512>(acc, smem, m0, n0, wm, wn, tid, Mv, N, ea);
+    epilogue_staged<BM, BN, EPI, WM, WN, 512>(acc, smem, m0, n0, grp, q, tid, Mv, N, ea);
   else
-    epilogue_w<BM, BN, EPI, WM, WN>(acc, m0, n0, wm, wn, lane, Mv, N, ea);
+    epilogue_w<BM, BN, EPI, WM, WN>(acc, m0, n0, grp, q, lane, Mv, N, ea);
 }
 
-template <int BM, int BN, int EPI>
-void launch_w8(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int K,
+template <int EPI>
+void launch_pp(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int K,
                const int* M_dev, const EpiArgs& ea) {
-  const int n_tm = ceil_div(M, BM), n_tn = ceil_div(N, BN);
-  gemm_bf16_w8_kernel<BM, BN, EPI><<<dim3(n_tm * n_tn), dim3(512), 0, st>>>(A, B, M, N, K, M_dev, ea, n_tm, n_tn);
+  const int n_tm = ceil_div(M, 256), n_tn = ceil_div(N, 256);
+  gemm_bf16_pp_kernel<EPI><<<dim3(n_tm * n_tn), dim3(512), 0, st>>>(A, B, M, N, K, M_dev, ea, n_tm, n_tn);
   DLMC_HIP(hipGetLastError());
 }
 
@@ -610,15 +638,14 @@ void launch_epi(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, 
   DLMC_HIP(hipGetLastError());
 }
 
-template <int BM, int BN>
-void launch_waves8(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int K,
-                   const int* M_dev, EpiKind epi, const EpiArgs& ea) {
+void launch_pingpong(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int K,
+                     const int* M_dev, EpiKind epi, const EpiArgs& ea) {
   switch (epi) {
-    case EPI_STORE_F32: launch_w8<BM, BN, EPI_STORE_F32>(st, A, B, M, N, K, M_dev, ea); break;
-    case EPI_RESIDUAL: launch_w8<BM, BN, EPI_RESIDUAL>(st, A, B, M, N, K, M_dev, ea); break;
-    case EPI_GELU: launch_w8<BM, BN, EPI_GELU>(st, A, B, M, N, K, M_dev, ea); break;
-    case EPI_QKV_ROPE: launch_w8<BM, BN, EPI_QKV_ROPE>(st, A, B, M, N, K, M_dev, ea); break;
-    case EPI_SWIGLU: launch_w8<BM, BN, EPI_SWIGLU>(st, A, B, M, N, K, M_dev, ea); break;
+    case EPI_STORE_F32: launch_pp<EPI_STORE_F32>(st, A, B, M, N, K, M_dev, ea); break;
+    case EPI_RESIDUAL: launch_pp<EPI_RESIDUAL>(st, A, B, M, N, K, M_dev, ea); break;
+    case EPI_GELU: launch_pp<EPI_GELU>(st, A, B, M, N, K, M_dev, ea); break;
+    case EPI_QKV_ROPE: launch_pp<EPI_QKV_ROPE>(st, A, B, M, N, K, M_dev, ea); break;
+    case EPI_SWIGLU: launch_pp<EPI_SWIGLU>(st, A, B, M, N, K, M_dev, ea); break;
   }
 }
 
@@ -658,7 +685,7 @@ void gemm_bf16(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, i
   // with the weights streamed from HBM as in a layer loop:
   //  - LM head (fp32 store): 4-wave 256 x 256 when enough rows are live;
   //  - at least three 256 x 256 tiles per CU (the SwiGLU FFN-in GEMM): the
-  //    8-wave 256 x 256 kernel;
+  //    8-wave 256 x 256 ping-pong kernel;
   //  - otherwise 4-wave 128 x 128 (two blocks per CU).
   const int live = rows_hint >= 0 ? std::min(rows_hint, M) : M;
   if (epi == EPI_STORE_F32) {
@@ -667,7 +694,7 @@ void gemm_bf16(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, i
     else
       launch<128, 128>(st, A, B, M, N, K, M_dev, epi, ea);
   } else if (N % 256 == 0 && (long)ceil_div(live, 256) * (N / 256) >= 3 * 256) {
-    launch_waves8<256, 256>(st, A, B, M, N, K, M_dev, epi, ea);
+    launch_pingpong(st, A, B, M, N, K, M_dev, epi, ea);
   } else {
     launch<128, 128>(st, A, B, M, N, K, M_dev, epi, ea);
   }
