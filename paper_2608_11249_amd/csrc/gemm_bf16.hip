@@ -144,7 +144,9 @@ __device__ __forceinline__ void epilogue(f32x16 (&acc)[BM / 64][BN / 64], int m0
 // transposed ([dh, Tp] per head).  Rows of an LDS tile carry 8 elements of
 // padding, which puts the two row groups a wave writes at once on different
 // banks.
-template <int BM, int BN, int EPI>
+// MAIN: LDS bytes of the main loop; BPC: blocks per CU the registers allow
+// (0: as many as the main loop's LDS allows).
+template <int BM, int BN, int EPI, int MAIN = 2 * (BM + BN) * BK * 2, int BPC = 0>
 struct StagedEpi {
   static constexpr int PF = BN + 8;       // fp32 tile pitch (STORE, RESIDUAL)
   static constexpr int PB = BN + 8;       // bf16 tile pitch (GELU, Q/K)
@@ -155,11 +157,11 @@ struct StagedEpi {
       : EPI == EPI_GELU                              ? BM * PB * 2
       : EPI == EPI_SWIGLU                            ? BM * PS * 2
       : (BM * PB > BN * PV ? BM * PB : BN * PV) * 2;
-  static constexpr int main_bytes = 2 * (BM + BN) * BK * 2;
+  static constexpr int main_bytes = MAIN;
   // staged only where it keeps the blocks-per-CU count of the main loop
   static constexpr int lds_cu = 160 * 1024;
-  static constexpr bool enabled =
-      bytes <= lds_cu && lds_cu / (bytes > main_bytes ? bytes : main_bytes) == lds_cu / main_bytes;
+  static constexpr int bpc = BPC > 0 && BPC < lds_cu / main_bytes ? BPC : lds_cu / main_bytes;
+  static constexpr bool enabled = bytes <= lds_cu && lds_cu / (bytes > main_bytes ? bytes : main_bytes) >= bpc;
   static constexpr int smem_elems = (enabled && bytes > main_bytes ? bytes : main_bytes) / 2;
 };
 
@@ -167,7 +169,7 @@ template <int BM, int BN, int EPI, int WM, int WN, int NT>
 __device__ __forceinline__ void epilogue_staged(f32x16 (&acc)[WM / 32][WN / 32], bf16_t* smem,
                                                 int m0, int n0, int wm, int wn, int tid, int Mv,
                                                 int N, const EpiArgs& ea) {
-  using SE = StagedEpi<BM, BN, EPI>;
+  using SE = StagedEpi<BM, BN, EPI>;  // pitches only: they do not depend on MAIN / BPC
   constexpr int TM = WM / 32, TN = WN / 32;
   const int lane = tid & 63, lr = lane & 31, lg = lane >> 5;
   const int wr0 = wm * WM, wc0 = wn * WN;  // wave tile origin inside the block tile
@@ -532,13 +534,18 @@ __device__ __forceinline__ void pp_issue_clamped(const bf16_t* __restrict__ A, i
   }
 }
 
-template <int EPI>
+// NSB: LDS stages of the B (weight) tile.  With 3 (and 2 for A, 160 KB in
+// all) group 0 issues weight tile k + 2 with activation tile k + 1, which
+// doubles the time the weight loads have to arrive from HBM.
+template <int EPI, int NSB>
 __global__ void __launch_bounds__(512)
 gemm_bf16_pp_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, int M, int N,
                     int K, const int* __restrict__ M_dev, EpiArgs ea, int n_tm, int n_tn) {
   constexpr int BM = 256, BN = 256, WM = 128, WN = 64, TM = WM / 32, TN = WN / 32;
   constexpr int A_IN = BM / 32, B_IN = BN / 32;  // 1 KB direct loads per group-0 wave per k-tile
-  __shared__ __attribute__((aligned(16))) bf16_t smem[StagedEpi<BM, BN, EPI>::smem_elems];
+  static_assert(NSB == 2 || NSB == 3, "two or three weight stages");
+  using SE = StagedEpi<BM, BN, EPI, (2 * BM + NSB * BN) * BK * 2, 1>;
+  __shared__ __attribute__((aligned(16))) bf16_t smem[SE::smem_elems];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, kept scalar
@@ -563,14 +570,15 @@ gemm_bf16_pp_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw,
   const bf16_t* a_src = A + (size_t)m0 * K;
   const bf16_t* b_src = Bw + (size_t)n0 * K;
   const int a_win = q * A_IN * 512, b_win = q * B_IN * 512;
-  auto issue = [&](int kt, int stage) {
-    bf16_t* as = As + stage * BM * BK + a_win;
-    bf16_t* bs = Bs + stage * BN * BK + b_win;
+  auto issue_a = [&](int kt) {
+    bf16_t* as = As + (kt & 1) * BM * BK + a_win;
     if (a_full)
       pp_issue<A_IN>(a_src + kt * BK, off, stride8, as);
     else
       pp_issue_clamped<A_IN>(A, m0 + lrow, Mv - 1, K, kt * BK, lrow, lane, as);
-    pp_issue<B_IN>(b_src + kt * BK, off, stride8, bs);
+  };
+  auto issue_b = [&](int kt) {
+    pp_issue<B_IN>(b_src + kt * BK, off, stride8, Bs + (kt % NSB) * BN * BK + b_win);
   };
 
   f32x16 acc[TM][TN];
@@ -582,18 +590,32 @@ gemm_bf16_pp_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw,
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
   const int nk = K / BK;
+  // vmcnt waits: 0x0F70 = vmcnt(0); 0x0F70 | B_IN leaves the last B_IN loads
+  // (the weight tile issued two ahead) in flight
+  constexpr int WAIT_ALL = 0x0F70, WAIT_B_AHEAD = 0x0F70 | B_IN;
+  static_assert(B_IN < 16, "vmcnt field");
   if (grp == 0) {
-    issue(0, 0);
-    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+    issue_a(0);
+    issue_b(0);
+    if (NSB == 3 && nk > 1) {
+      issue_b(1);
+      __builtin_amdgcn_s_waitcnt(WAIT_B_AHEAD);
+    } else {
+      __builtin_amdgcn_s_waitcnt(WAIT_ALL);
+    }
   }
   pp_barrier();
   if (grp == 1) pp_barrier();  // group 1 runs one phase behind
   for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
     // memory phase
-    if (grp == 0 && kt + 1 < nk) issue(kt + 1, cur ^ 1);
-    const bf16_t* as = As + cur * BM * BK;
-    const bf16_t* bs = Bs + cur * BN * BK;
+    const bool b_ahead = NSB == 3 && kt + 2 < nk;
+    if (grp == 0) {
+      if (kt + 1 < nk) issue_a(kt + 1);
+      if (NSB == 2 && kt + 1 < nk) issue_b(kt + 1);
+      if (b_ahead) issue_b(kt + 2);
+    }
+    const bf16_t* as = As + (kt & 1) * BM * BK;
+    const bf16_t* bs = Bs + (kt % NSB) * BN * BK;
     bf16x8 fa[4][TM], fb[4][TN];
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
@@ -612,21 +634,27 @@ gemm_bf16_pp_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw,
         for (int j = 0; j < TN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s][j], acc[i][j], 0, 0, 0);
     __builtin_amdgcn_s_setprio(0);
-    if (grp == 0) __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): tile kt + 1 has landed
+    // tiles kt + 1 of A and B have landed (the weight tile kt + 2 may not)
+    if (grp == 0) {
+      if (b_ahead)
+        __builtin_amdgcn_s_waitcnt(WAIT_B_AHEAD);
+      else
+        __builtin_amdgcn_s_waitcnt(WAIT_ALL);
+    }
     pp_barrier();
   }
   if (grp == 0) pp_barrier();  // both groups have passed the same number of barriers
-  if constexpr (StagedEpi<BM, BN, EPI>::enabled)
+  if constexpr (SE::enabled)
     epilogue_staged<BM, BN, EPI, WM, WN, 512>(acc, smem, m0, n0, grp, q, tid, Mv, N, ea);
   else
     epilogue_w<BM, BN, EPI, WM, WN>(acc, m0, n0, grp, q, lane, Mv, N, ea);
 }
 
-template <int EPI>
+template <int EPI, int NSB = 3>
 void launch_pp(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int K,
                const int* M_dev, const EpiArgs& ea) {
   const int n_tm = ceil_div(M, 256), n_tn = ceil_div(N, 256);
-  gemm_bf16_pp_kernel<EPI><<<dim3(n_tm * n_tn), dim3(512), 0, st>>>(A, B, M, N, K, M_dev, ea, n_tm, n_tn);
+  gemm_bf16_pp_kernel<EPI, NSB><<<dim3(n_tm * n_tn), dim3(512), 0, st>>>(A, B, M, N, K, M_dev, ea, n_tm, n_tn);
   DLMC_HIP(hipGetLastError());
 }
 
@@ -683,14 +711,15 @@ void gemm_bf16(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, i
              DLMC_E_INVAL, "QKV epilogue needs d % 128 == 0 and head dim 64 or 128");
   // Tile choice (never changes the result), from measurements at M = 2048
   // with the weights streamed from HBM as in a layer loop:
-  //  - LM head (fp32 store): 4-wave 256 x 256 when enough rows are live;
+  //  - LM head (fp32 store): the 8-wave 256 x 256 ping-pong kernel when
+  //    enough rows are live;
   //  - at least three 256 x 256 tiles per CU (the SwiGLU FFN-in GEMM): the
   //    8-wave 256 x 256 ping-pong kernel;
   //  - otherwise 4-wave 128 x 128 (two blocks per CU).
   const int live = rows_hint >= 0 ? std::min(rows_hint, M) : M;
   if (epi == EPI_STORE_F32) {
     if (N % 256 == 0 && live >= 512)
-      launch<256, 256>(st, A, B, M, N, K, M_dev, epi, ea);
+      launch_pingpong(st, A, B, M, N, K, M_dev, epi, ea);
     else
       launch<128, 128>(st, A, B, M, N, K, M_dev, epi, ea);
   } else if (N % 256 == 0 && (long)ceil_div(live, 256) * (N / 256) >= 3 * 256) {
