@@ -119,6 +119,61 @@ norm_kernel(const float* __restrict__ x, void* __restrict__ out, int out_dtype, 
   }
 }
 
+// Same normalisation with 16-byte loads: thread t holds columns 4 (t + 256 e)
+// .. + 3 (d % 1024 == 0), and writes them as one 8-byte (bf16) or 16-byte
+// store.
+template <int PER4>
+__global__ void __launch_bounds__(256)
+norm4_kernel(const float* __restrict__ x, void* __restrict__ out, int out_dtype, int d,
+             int norm_kind, float eps, const int32_t* __restrict__ gather,
+             const int32_t* __restrict__ n_dev) {
+  __shared__ float red[4];
+  const int i = blockIdx.x;
+  if (n_dev && i >= *n_dev) return;
+  const int src = gather ? gather[i] : i;
+  const float4* xr = reinterpret_cast<const float4*>(x + (size_t)src * d);
+  float4 v[PER4];
+#pragma unroll
+  for (int e = 0; e < PER4; ++e) v[e] = xr[threadIdx.x + 256 * e];
+  float scale, shift = 0.0f;
+  if (norm_kind == DLMC_NORM_LAYER) {
+    float s = 0.0f;
+#pragma unroll
+    for (int e = 0; e < PER4; ++e) s += (v[e].x + v[e].y) + (v[e].z + v[e].w);
+    const float mean = block_sum256(s, red) / (float)d;
+    float q = 0.0f;
+#pragma unroll
+    for (int e = 0; e < PER4; ++e) {
+      const float a = v[e].x - mean, b = v[e].y - mean, c = v[e].z - mean, w = v[e].w - mean;
+      q += (a * a + b * b) + (c * c + w * w);
+    }
+    const float var = block_sum256(q, red) / (float)d;
+    scale = 1.0f / sqrtf(var + eps);
+    shift = mean;
+  } else {
+    float s = 0.0f;
+#pragma unroll
+    for (int e = 0; e < PER4; ++e)
+      s += (v[e].x * v[e].x + v[e].y * v[e].y) + (v[e].z * v[e].z + v[e].w * v[e].w);
+    const float ms = block_sum256(s, red) / (float)d;
+    scale = 1.0f / sqrtf(ms + eps);
+  }
+#pragma unroll
+  for (int e = 0; e < PER4; ++e) {
+    const int c4 = threadIdx.x + 256 * e;
+    const float y0 = (v[e].x - shift) * scale, y1 = (v[e].y - shift) * scale;
+    const float y2 = (v[e].z - shift) * scale, y3 = (v[e].w - shift) * scale;
+    if (out_dtype == DLMC_DTYPE_BF16) {
+      u32x2 w;
+      w[0] = (uint32_t)f32_to_bf16(y0) | ((uint32_t)f32_to_bf16(y1) << 16);
+      w[1] = (uint32_t)f32_to_bf16(y2) | ((uint32_t)f32_to_bf16(y3) << 16);
+      reinterpret_cast<u32x2*>((bf16_t*)out + (size_t)i * d)[c4] = w;
+    } else {
+      reinterpret_cast<float4*>((float*)out + (size_t)i * d)[c4] = make_float4(y0, y1, y2, y3);
+    }
+  }
+}
+
 __global__ void fill_kernel(int32_t* p, int32_t v, size_t n) {
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
        i += (size_t)gridDim.x * blockDim.x)
@@ -259,6 +314,24 @@ void norm_rows(hipStream_t st, const float* x, void* out, int out_dtype, int n_r
   if (n_rows <= 0) return;
   const int per = ceil_div(d, 256);
   dim3 grid(n_rows), block(256);
+  if (d % 1024 == 0 && d <= 8192) {
+#define DLMC_NORM4(P)                                                                           \
+  norm4_kernel<P><<<grid, block, 0, st>>>(x, out, out_dtype, d, norm_kind, eps, gather_rows, \
+                                          n_dev)
+    switch (d / 1024) {
+      case 1: DLMC_NORM4(1); break;
+      case 2: DLMC_NORM4(2); break;
+      case 3: DLMC_NORM4(3); break;
+      case 4: DLMC_NORM4(4); break;
+      case 5: DLMC_NORM4(5); break;
+      case 6: DLMC_NORM4(6); break;
+      case 7: DLMC_NORM4(7); break;
+      default: DLMC_NORM4(8); break;
+    }
+#undef DLMC_NORM4
+    DLMC_HIP(hipGetLastError());
+    return;
+  }
 #define DLMC_NORM(P)                                                                           \
   norm_kernel<P><<<grid, block, 0, st>>>(x, out, out_dtype, d, norm_kind, eps, gather_rows, \
                                          n_dev)

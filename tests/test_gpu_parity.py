@@ -93,6 +93,13 @@ def test_logits_bf16_small_shapes(kw, B, T):
     check_logits(shape(**kw), B, T, 0.6, 2e-2)
 
 
+@pytest.mark.parametrize("kw", [dict(ffn="swiglu", norm="rmsnorm"), dict(ffn="gelu", norm="layernorm")])
+def test_logits_bf16_wide_rows(kw):
+    """d_model = 1024 takes the 16-byte-load norm kernel (both norm kinds)."""
+    sh = shape(d_model=1024, n_heads=8, d_ffn=1024, n_layers=1, vocab=300, **kw)
+    check_logits(sh, 2, 96, 0.6, 2e-2)
+
+
 def test_logits_bf16_pingpong_ragged_rows():
     """A wide SwiGLU FFN (2F = 98304 columns) puts the FFN-in GEMM on the
     8-wave 256 x 256 ping-pong kernel; 300 rows leave its second row tile
