@@ -8,15 +8,18 @@
 // fragment loads are free of bank conflicts.  Two kernels:
 //  - gemm_bf16_kernel: four waves in a 2 x 2 grid, one barrier per k-tile,
 //    the fragment reads of k step s + 1 scheduled between the MFMAs of step s
-//    (128 x 128 tiles, two blocks per CU, and the 256 x 256 LM head);
-//  - gemm_bf16_pp_kernel: eight waves on a 256 x 256 tile in two groups that
-//    alternate memory and compute phases (the SwiGLU FFN-in GEMM).
+//    (128 x 128 tiles, two blocks per CU);
+//  - gemm_bf16_w4_kernel: four waves, one per SIMD, on a 256 x 256 tile
+//    with 128 x 128 wave tiles, A double- and B triple-buffered in LDS
+//    (the SwiGLU FFN-in GEMM and the LM head).
 //
 // Numerics: each output element is a sequential sum over k-tiles, each k-tile
 // four MFMA steps in order, independent of the kernel, the tile shape and of
 // which other rows are in the launch, so results are identical for any batch
 // composition.
 #include "kernels.h"
+
+#include <type_traits>
 
 namespace dlmc {
 namespace {
@@ -486,25 +489,30 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, in
 }
 
 // ---------------------------------------------------------------------------
-// 8-wave 256 x 256 kernel with a ping-pong schedule.
+// 4-wave 256 x 256 kernel: one wave per SIMD, each wave a 128 x 128 sub-tile
+// (16 accumulator tiles, 256 AGPRs), so each k step reads 8 fragments for 16
+// MFMAs -- half the LDS reads per flop of a 128 x 64 wave tile.
 //
-// The two waves of a SIMD belong to different groups (waves 0-3 and 4-7)
-// that run one phase apart.  Per k-tile each group has a memory phase (all 24
-// MFMA fragments of the wave's 128 x 64 sub-tile read from LDS into
-// registers; group 0 also issues the direct loads of the next k-tile) and a
-// compute phase (the wave's 32 MFMAs back to back from registers, at raised
-// wave priority).  Every phase ends at a workgroup barrier, so on each SIMD
-// one wave computes while the other loads, and the MFMA pipe is fed from
-// registers instead of waiting on LDS reads, load completion and barriers.
+// LDS stages: A (activation) tile k sits in stage k % 2, B (weight) tile k in
+// stage k % 3 (160 KB in all).  One barrier per k-tile, between k steps 2 and
+// 3: before it each wave has waited for its own direct loads of tile k + 1 and
+// for its fragment reads of tile k; after it, tile k's stages are free, so
+// the loads of tile k + 2 (A and B) go into them while step 3 runs.  A tile
+// k + 1 is thus issued half under step 3 of k-tile k - 1 and half under step 0
+// of k-tile k, B tile k + 2 under steps 1 and 2 of k-tile k, so the weight
+// tile has about two k-tiles to arrive from HBM.
 //
-// LDS stages: tile k sits in stage k % 2.  Group 0 issues tile k + 1 at the
-// start of its memory phase for tile k and waits for it at the end of its
-// compute phase; both groups finish reading tile k (their memory phases,
-// which end with every LDS read landed) before group 0 starts tile k + 2.
+// Each k step runs as four chunks in a fixed order, split by scheduling
+// barriers: one direct load (when one is due), the next step's fragment reads
+// (the first two chunks), four MFMAs.  The direct loads of a k-tile are thus
+// spread evenly over it, one per four MFMAs per wave; issued in bursts they
+// back up the load path and hold up the MFMAs behind them.
 //
 // Numerics: each accumulator takes the k steps of each k-tile in order, as in
-// gemm_bf16_kernel, so the results are identical to the other kernels'.
-__device__ __forceinline__ void pp_barrier() {
+// gemm_bf16_kernel, so the results are identical to the other kernel's.
+__device__ __forceinline__ void block_barrier() {
+  // s_barrier without the memory fence of __syncthreads(), which would also
+  // wait for the direct loads still in flight
   __builtin_amdgcn_sched_barrier(0);
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_barrier();
@@ -512,44 +520,18 @@ __device__ __forceinline__ void pp_barrier() {
   __builtin_amdgcn_sched_barrier(0);
 }
 
-// Direct loads of one k-tile by a group-0 wave: 8 windows of A rows and 8 of
-// B rows (rows 64 q .. 64 q + 63 of each tile).  Window j covers rows 8 j ..
-// 8 j + 7 of the wave's range; its chunk swizzle depends only on j % 2, so
-// two per-lane offsets (off[0], off[1]) serve all windows.  A tile that runs
-// past the live rows (Mv) takes clamped row indices instead.
-template <int NWIN>
-__device__ __forceinline__ void pp_issue(const bf16_t* __restrict__ src, const int (&off)[2],
-                                         size_t row_stride8, bf16_t* lds) {
-#pragma unroll
-  for (int j = 0; j < NWIN; ++j) lds_dma16(src + j * row_stride8 + off[j & 1], lds + j * 512);
-}
-template <int NWIN>
-__device__ __forceinline__ void pp_issue_clamped(const bf16_t* __restrict__ A, int first_row,
-                                                 int last_row, int K, int col, int lrow, int lane,
-                                                 bf16_t* lds) {
-#pragma unroll
-  for (int j = 0; j < NWIN; ++j) {
-    const int chunk = ((lane & 7) ^ swz(lrow + 8 * (j & 1))) << 3;
-    lds_dma16(A + (min(first_row + 8 * j, last_row) * K + col + chunk), lds + j * 512);
-  }
-}
-
-// NSB: LDS stages of the B (weight) tile.  With 3 (and 2 for A, 160 KB in
-// all) group 0 issues weight tile k + 2 with activation tile k + 1, which
-// doubles the time the weight loads have to arrive from HBM.
-template <int EPI, int NSB>
-__global__ void __launch_bounds__(512)
-gemm_bf16_pp_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, int M, int N,
+template <int EPI>
+__global__ void __launch_bounds__(256)
+gemm_bf16_w4_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, int M, int N,
                     int K, const int* __restrict__ M_dev, EpiArgs ea, int n_tm, int n_tn) {
-  constexpr int BM = 256, BN = 256, WM = 128, WN = 64, TM = WM / 32, TN = WN / 32;
-  constexpr int A_IN = BM / 32, B_IN = BN / 32;  // 1 KB direct loads per group-0 wave per k-tile
-  static_assert(NSB == 2 || NSB == 3, "two or three weight stages");
+  constexpr int BM = 256, BN = 256, WM = 128, WN = 128, TM = WM / 32, TN = WN / 32, NSB = 3;
+  constexpr int A_IN = BM / 32, B_IN = BN / 32;  // 1 KB direct loads per wave per k-tile
   using SE = StagedEpi<BM, BN, EPI, (2 * BM + NSB * BN) * BK * 2, 1>;
   __shared__ __attribute__((aligned(16))) bf16_t smem[SE::smem_elems];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, kept scalar
-  const int grp = wave >> 2, q = wave & 3;  // wave q of group grp owns rows 128 grp, columns 64 q
+  const int wm = wave >> 1, wn = wave & 1;
   const int lr = lane & 31, lg = lane >> 5;
   const int Mv = M_dev ? min(*M_dev, M) : M;
   int tm, tn;
@@ -559,26 +541,27 @@ gemm_bf16_pp_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw,
 
   bf16_t* As = smem;
   bf16_t* Bs = smem + 2 * BM * BK;
-  // group-0 direct loads: lane l of window j fills row 64 q + 8 j + l / 8,
-  // 16-byte slot l % 8, with chunk (l % 8) ^ swz(row) of that row
-  const int lrow = 64 * q + (lane >> 3);
+  // direct loads: window j of wave w fills tile rows 64 w + 8 j .. + 7 (1 KB);
+  // lane l fills row 64 w + 8 j + l / 8, 16-byte slot l % 8, with chunk
+  // (l % 8) ^ swz(row) of that row.  The swizzle depends only on j % 2.  A rows
+  // past the live rows (Mv) are clamped; N % 256 == 0 keeps B tiles whole.
+  const int lrow = 64 * wave + (lane >> 3);
   int off[2];
 #pragma unroll
   for (int e = 0; e < 2; ++e) off[e] = lrow * K + (((lane & 7) ^ swz(lrow + 8 * e)) << 3);
-  const bool a_full = m0 + BM <= Mv;  // N % 256 == 0: B tiles are always whole
   const size_t stride8 = (size_t)8 * K;
-  const bf16_t* a_src = A + (size_t)m0 * K;
   const bf16_t* b_src = Bw + (size_t)n0 * K;
-  const int a_win = q * A_IN * 512, b_win = q * B_IN * 512;
-  auto issue_a = [&](int kt) {
-    bf16_t* as = As + (kt & 1) * BM * BK + a_win;
-    if (a_full)
-      pp_issue<A_IN>(a_src + kt * BK, off, stride8, as);
-    else
-      pp_issue_clamped<A_IN>(A, m0 + lrow, Mv - 1, K, kt * BK, lrow, lane, as);
+  const int a_win = wave * A_IN * 512, b_win = wave * B_IN * 512;
+  auto dma_a = [&](int kt, int j) {
+    const int chunk = ((lane & 7) ^ swz(lrow + 8 * (j & 1))) << 3;
+    lds_dma16(A + (min(m0 + lrow + 8 * j, Mv - 1) * K + kt * BK + chunk),
+              As + (kt & 1) * BM * BK + a_win + j * 512);
   };
-  auto issue_b = [&](int kt) {
-    pp_issue<B_IN>(b_src + kt * BK, off, stride8, Bs + (kt % NSB) * BN * BK + b_win);
+  auto dma_b = [&](int kt, int j) {
+    lds_dma16(b_src + kt * BK + j * stride8 + off[j & 1], Bs + (kt % NSB) * BN * BK + b_win + j * 512);
+  };
+  auto frag = [&](bf16x8& f, const bf16_t* base, int row, int kc) {
+    f = *reinterpret_cast<const bf16x8*>(base + row * BK + ((kc ^ swz(row)) << 3));
   };
 
   f32x16 acc[TM][TN];
@@ -590,71 +573,101 @@ gemm_bf16_pp_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw,
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
   const int nk = K / BK;
-  // vmcnt waits: 0x0F70 = vmcnt(0); 0x0F70 | B_IN leaves the last B_IN loads
-  // (the weight tile issued two ahead) in flight
-  constexpr int WAIT_ALL = 0x0F70, WAIT_B_AHEAD = 0x0F70 | B_IN;
+  // s_waitcnt encodings: vmcnt(0) / vmcnt(B_IN), each with lgkmcnt(0)
+  constexpr int WAIT_ALL = 0x0070, WAIT_B_AHEAD = 0x0070 | B_IN;
   static_assert(B_IN < 16, "vmcnt field");
-  if (grp == 0) {
-    issue_a(0);
-    issue_b(0);
-    if (NSB == 3 && nk > 1) {
-      issue_b(1);
-      __builtin_amdgcn_s_waitcnt(WAIT_B_AHEAD);
-    } else {
-      __builtin_amdgcn_s_waitcnt(WAIT_ALL);
-    }
+#pragma unroll
+  for (int j = 0; j < A_IN; ++j) dma_a(0, j);
+#pragma unroll
+  for (int j = 0; j < B_IN; ++j) dma_b(0, j);
+  if (nk > 1) {
+#pragma unroll
+    for (int j = 0; j < B_IN; ++j) dma_b(1, j);
+    __builtin_amdgcn_s_waitcnt(WAIT_B_AHEAD);
+  } else {
+    __builtin_amdgcn_s_waitcnt(WAIT_ALL);
   }
-  pp_barrier();
-  if (grp == 1) pp_barrier();  // group 1 runs one phase behind
-  for (int kt = 0; kt < nk; ++kt) {
-    // memory phase
-    const bool b_ahead = NSB == 3 && kt + 2 < nk;
-    if (grp == 0) {
-      if (kt + 1 < nk) issue_a(kt + 1);
-      if (NSB == 2 && kt + 1 < nk) issue_b(kt + 1);
-      if (b_ahead) issue_b(kt + 2);
-    }
-    const bf16_t* as = As + (kt & 1) * BM * BK;
-    const bf16_t* bs = Bs + (kt % NSB) * BN * BK;
-    bf16x8 fa[4][TM], fb[4][TN];
+  block_barrier();
+  if (nk > 1) {
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      load_frags<TM>(fa[s], as, grp * WM, lr, 2 * s + lg);
-      load_frags<TN>(fb[s], bs, q * WN, lr, 2 * s + lg);
-    }
-    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave is done with the stage
-    pp_barrier();
-    // compute phase
-    __builtin_amdgcn_s_setprio(1);
+    for (int j = 0; j < A_IN / 2; ++j) dma_a(1, j);
+  }
+  bf16x8 fa[2][TM], fb[2][TN];
+  load_frags<TM>(fa[0], As, wm * WM, lr, lg);
+  load_frags<TN>(fb[0], Bs, wn * WN, lr, lg);
+
+  // one k-tile.  X: A tile kt + 1 exists (its second half is issued in step
+  // 0); Y: tile kt + 2 exists (B in steps 1 and 2, the first half of A in
+  // step 3).
+  auto trip = [&](int kt, auto x_, auto y_) {
+    constexpr bool X = decltype(x_)::value, Y = decltype(y_)::value;
+    // k step S: MFMAs on fragment set S % 2 while the other set is read from
+    // (an, bn) at 16-byte chunk kc
+    auto step = [&](auto s_, const bf16_t* an, const bf16_t* bn, int kc) {
+      constexpr int S = decltype(s_)::value, c = S & 1;
+      auto chunk = [&](auto q_) {
+        constexpr int Q = decltype(q_)::value;
+        if constexpr (S == 0 && X) dma_a(kt + 1, A_IN / 2 + Q);
+        if constexpr (S == 1 && Y) dma_b(kt + 2, Q);
+        if constexpr (S == 2 && Y) dma_b(kt + 2, B_IN / 2 + Q);
+        if constexpr (S == 3 && Y) dma_a(kt + 2, Q);
+        // the next step's first MFMAs need A fragment 0 and every B fragment
+        if constexpr (Q == 0) {
 #pragma unroll
-    for (int s = 0; s < 4; ++s)
+          for (int e = 0; e < TN; ++e) frag(fb[c ^ 1][e], bn, wn * WN + e * 32 + lr, kc);
+          frag(fa[c ^ 1][0], an, wm * WM + lr, kc);
+        } else if constexpr (Q == 1) {
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
+          for (int e = 1; e < TM; ++e) frag(fa[c ^ 1][e], an, wm * WM + e * 32 + lr, kc);
+        }
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s][j], acc[i][j], 0, 0, 0);
-    __builtin_amdgcn_s_setprio(0);
-    // tiles kt + 1 of A and B have landed (the weight tile kt + 2 may not)
-    if (grp == 0) {
-      if (b_ahead)
-        __builtin_amdgcn_s_waitcnt(WAIT_B_AHEAD);
-      else
-        __builtin_amdgcn_s_waitcnt(WAIT_ALL);
-    }
-    pp_barrier();
+          acc[Q][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[c][Q], fb[c][j], acc[Q][j], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      };
+      static_assert(TM == 4 && A_IN == 8 && B_IN == 8, "four chunks per k step");
+      chunk(std::integral_constant<int, 0>{});
+      chunk(std::integral_constant<int, 1>{});
+      chunk(std::integral_constant<int, 2>{});
+      chunk(std::integral_constant<int, 3>{});
+    };
+    const bf16_t* as = As + (kt & 1) * BM * BK;
+    const bf16_t* bs = Bs + (kt % NSB) * BN * BK;
+    step(std::integral_constant<int, 0>{}, as, bs, 2 + lg);
+    step(std::integral_constant<int, 1>{}, as, bs, 4 + lg);
+    step(std::integral_constant<int, 2>{}, as, bs, 6 + lg);
+    // A tile kt + 1 (and B tile kt + 1, issued earlier) have landed; only B
+    // tile kt + 2 may still be in flight
+    if constexpr (Y)
+      __builtin_amdgcn_s_waitcnt(WAIT_B_AHEAD);
+    else
+      __builtin_amdgcn_s_waitcnt(WAIT_ALL);
+    block_barrier();
+    step(std::integral_constant<int, 3>{}, As + ((kt + 1) & 1) * BM * BK,
+         Bs + ((kt + 1) % NSB) * BN * BK, lg);
+  };
+  using T_ = std::true_type;
+  using F_ = std::false_type;
+  int kt = 0;
+  for (; kt + 2 < nk; ++kt) trip(kt, T_{}, T_{});
+  if (kt + 2 == nk) {
+    trip(kt, T_{}, F_{});
+    ++kt;
   }
-  if (grp == 0) pp_barrier();  // both groups have passed the same number of barriers
+  trip(kt, F_{}, F_{});  // its fragment reads past the last k-tile are unused
+  __builtin_amdgcn_s_waitcnt(WAIT_ALL);
+  block_barrier();
   if constexpr (SE::enabled)
-    epilogue_staged<BM, BN, EPI, WM, WN, 512>(acc, smem, m0, n0, grp, q, tid, Mv, N, ea);
+    epilogue_staged<BM, BN, EPI, WM, WN, 256>(acc, smem, m0, n0, wm, wn, tid, Mv, N, ea);
   else
-    epilogue_w<BM, BN, EPI, WM, WN>(acc, m0, n0, grp, q, lane, Mv, N, ea);
+    epilogue_w<BM, BN, EPI, WM, WN>(acc, m0, n0, wm, wn, lane, Mv, N, ea);
 }
 
-template <int EPI, int NSB = 3>
-void launch_pp(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int K,
+template <int EPI>
+void launch_w4(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int K,
                const int* M_dev, const EpiArgs& ea) {
   const int n_tm = ceil_div(M, 256), n_tn = ceil_div(N, 256);
-  gemm_bf16_pp_kernel<EPI, NSB><<<dim3(n_tm * n_tn), dim3(512), 0, st>>>(A, B, M, N, K, M_dev, ea, n_tm, n_tn);
+  gemm_bf16_w4_kernel<EPI><<<dim3(n_tm * n_tn), dim3(256), 0, st>>>(A, B, M, N, K, M_dev, ea, n_tm, n_tn);
   DLMC_HIP(hipGetLastError());
 }
 
@@ -666,14 +679,14 @@ void launch_epi(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, 
   DLMC_HIP(hipGetLastError());
 }
 
-void launch_pingpong(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int K,
-                     const int* M_dev, EpiKind epi, const EpiArgs& ea) {
+void launch_256(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int K,
+                const int* M_dev, EpiKind epi, const EpiArgs& ea) {
   switch (epi) {
-    case EPI_STORE_F32: launch_pp<EPI_STORE_F32>(st, A, B, M, N, K, M_dev, ea); break;
-    case EPI_RESIDUAL: launch_pp<EPI_RESIDUAL>(st, A, B, M, N, K, M_dev, ea); break;
-    case EPI_GELU: launch_pp<EPI_GELU>(st, A, B, M, N, K, M_dev, ea); break;
-    case EPI_QKV_ROPE: launch_pp<EPI_QKV_ROPE>(st, A, B, M, N, K, M_dev, ea); break;
-    case EPI_SWIGLU: launch_pp<EPI_SWIGLU>(st, A, B, M, N, K, M_dev, ea); break;
+    case EPI_STORE_F32: launch_w4<EPI_STORE_F32>(st, A, B, M, N, K, M_dev, ea); break;
+    case EPI_RESIDUAL: launch_w4<EPI_RESIDUAL>(st, A, B, M, N, K, M_dev, ea); break;
+    case EPI_GELU: launch_w4<EPI_GELU>(st, A, B, M, N, K, M_dev, ea); break;
+    case EPI_QKV_ROPE: launch_w4<EPI_QKV_ROPE>(st, A, B, M, N, K, M_dev, ea); break;
+    case EPI_SWIGLU: launch_w4<EPI_SWIGLU>(st, A, B, M, N, K, M_dev, ea); break;
   }
 }
 
@@ -711,19 +724,19 @@ void gemm_bf16(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, i
              DLMC_E_INVAL, "QKV epilogue needs d % 128 == 0 and head dim 64 or 128");
   // Tile choice (never changes the result), from measurements at M = 2048
   // with the weights streamed from HBM as in a layer loop:
-  //  - LM head (fp32 store): the 8-wave 256 x 256 ping-pong kernel when
-  //    enough rows are live;
+  //  - LM head (fp32 store): the 4-wave 256 x 256 kernel when enough rows
+  //    are live;
   //  - at least three 256 x 256 tiles per CU (the SwiGLU FFN-in GEMM): the
-  //    8-wave 256 x 256 ping-pong kernel;
+  //    4-wave 256 x 256 kernel;
   //  - otherwise 4-wave 128 x 128 (two blocks per CU).
   const int live = rows_hint >= 0 ? std::min(rows_hint, M) : M;
   if (epi == EPI_STORE_F32) {
     if (N % 256 == 0 && live >= 512)
-      launch_pingpong(st, A, B, M, N, K, M_dev, epi, ea);
+      launch_256(st, A, B, M, N, K, M_dev, epi, ea);
     else
       launch<128, 128>(st, A, B, M, N, K, M_dev, epi, ea);
   } else if (N % 256 == 0 && (long)ceil_div(live, 256) * (N / 256) >= 3 * 256) {
-    launch_pingpong(st, A, B, M, N, K, M_dev, epi, ea);
+    launch_256(st, A, B, M, N, K, M_dev, epi, ea);
   } else {
     launch<128, 128>(st, A, B, M, N, K, M_dev, epi, ea);
   }

@@ -100,10 +100,10 @@ def test_logits_bf16_wide_rows(kw):
     check_logits(sh, 2, 96, 0.6, 2e-2)
 
 
-def test_logits_bf16_pingpong_ragged_rows():
+def test_logits_bf16_256_tile_ragged_rows():
     """A wide SwiGLU FFN (2F = 98304 columns) puts the FFN-in GEMM on the
-    8-wave 256 x 256 ping-pong kernel; 300 rows leave its second row tile
-    ragged (44 live rows), which takes the clamped-load path."""
+    4-wave 256 x 256 kernel; 300 rows leave its second row tile ragged (44
+    live rows), whose loads clamp the row index."""
     sh = shape(d_model=128, n_heads=1, d_ffn=49152, ffn="swiglu", norm="rmsnorm", n_layers=1,
                vocab=300)
     check_logits(sh, 1, 300, 0.6, 2e-2)
