@@ -8,10 +8,10 @@
 // fragment loads are free of bank conflicts.  Two kernels:
 //  - gemm_bf16_kernel: four waves in a 2 x 2 grid, one barrier per k-tile,
 //    the fragment reads of k step s + 1 scheduled between the MFMAs of step s
-//    (128 x 128 tiles, two blocks per CU);
-//  - gemm_bf16_w4_kernel: four waves, one per SIMD, on a 256 x 256 tile
-//    with 128 x 128 wave tiles, A double- and B triple-buffered in LDS
-//    (the SwiGLU FFN-in GEMM and the LM head).
+//    (128 x 128 tiles, two blocks per CU; small and ragged shapes);
+//  - gemm_bf16_w4_kernel: four waves, one per SIMD, on a 256 x 256 or
+//    256 x 128 tile, A double- and B triple-buffered in LDS (every GEMM of
+//    the 8B-shaped pass).
 //
 // Numerics: each output element is a sequential sum over k-tiles, each k-tile
 // four MFMA steps in order, independent of the kernel, the tile shape and of
@@ -489,12 +489,15 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, in
 }
 
 // ---------------------------------------------------------------------------
-// 4-wave 256 x 256 kernel: one wave per SIMD, each wave a 128 x 128 sub-tile
-// (16 accumulator tiles, 256 AGPRs), so each k step reads 8 fragments for 16
-// MFMAs -- half the LDS reads per flop of a 128 x 64 wave tile.
+// 4-wave 256 x BN kernel (BN = 256 or 128): one wave per SIMD, each wave a
+// 128 x BN/2 sub-tile (up to 16 accumulator tiles, 256 AGPRs), so a k step
+// reads 8 fragments for 16 MFMAs at BN = 256.  The 256-row tile moves fewer
+// operand bytes through LDS per flop than 128 x 128 tiles (the direct loads
+// into LDS, not the MFMAs, are what limits those), and one block per CU
+// covers the narrower GEMMs in whole waves of tiles.
 //
 // LDS stages: A (activation) tile k sits in stage k % 2, B (weight) tile k in
-// stage k % 3 (160 KB in all).  One barrier per k-tile, between k steps 2 and
+// stage k % 3 (160 KB in all at BN = 256).  One barrier per k-tile, between k steps 2 and
 // 3: before it each wave has waited for its own direct loads of tile k + 1 and
 // for its fragment reads of tile k; after it, tile k's stages are free, so
 // the loads of tile k + 2 (A and B) go into them while step 3 runs.  A tile
@@ -503,10 +506,10 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, in
 // tile has about two k-tiles to arrive from HBM.
 //
 // Each k step runs as four chunks in a fixed order, split by scheduling
-// barriers: one direct load (when one is due), the next step's fragment reads
-// (the first two chunks), four MFMAs.  The direct loads of a k-tile are thus
-// spread evenly over it, one per four MFMAs per wave; issued in bursts they
-// back up the load path and hold up the MFMAs behind them.
+// barriers: the direct loads due (at most one of A, B_IN / 8 of B), the next
+// step's fragment reads (the first two chunks), BN / 64 MFMAs.  The direct
+// loads of a k-tile are thus spread evenly over it; issued in bursts they back
+// up the load path and hold up the MFMAs behind them.
 //
 // Numerics: each accumulator takes the k steps of each k-tile in order, as in
 // gemm_bf16_kernel, so the results are identical to the other kernel's.
@@ -520,11 +523,12 @@ __device__ __forceinline__ void block_barrier() {
   __builtin_amdgcn_sched_barrier(0);
 }
 
-template <int EPI>
+template <int EPI, int BN>
 __global__ void __launch_bounds__(256)
 gemm_bf16_w4_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, int M, int N,
                     int K, const int* __restrict__ M_dev, EpiArgs ea, int n_tm, int n_tn) {
-  constexpr int BM = 256, BN = 256, WM = 128, WN = 128, TM = WM / 32, TN = WN / 32, NSB = 3;
+  static_assert(BN == 256 || BN == 128, "256 x 256 or 256 x 128 tiles");
+  constexpr int BM = 256, WM = 128, WN = BN / 2, TM = WM / 32, TN = WN / 32, NSB = 3;
   constexpr int A_IN = BM / 32, B_IN = BN / 32;  // 1 KB direct loads per wave per k-tile
   using SE = StagedEpi<BM, BN, EPI, (2 * BM + NSB * BN) * BK * 2, 1>;
   __shared__ __attribute__((aligned(16))) bf16_t smem[SE::smem_elems];
@@ -541,14 +545,16 @@ gemm_bf16_w4_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw,
 
   bf16_t* As = smem;
   bf16_t* Bs = smem + 2 * BM * BK;
-  // direct loads: window j of wave w fills tile rows 64 w + 8 j .. + 7 (1 KB);
-  // lane l fills row 64 w + 8 j + l / 8, 16-byte slot l % 8, with chunk
-  // (l % 8) ^ swz(row) of that row.  The swizzle depends only on j % 2.  A rows
-  // past the live rows (Mv) are clamped; N % 256 == 0 keeps B tiles whole.
+  // direct loads: window j of wave w fills A tile rows 64 w + 8 j .. + 7 (1 KB)
+  // or B tile rows (BN / 4) w + 8 j .. + 7; lane l fills row 8 j + l / 8 of the
+  // wave's range, 16-byte slot l % 8, with chunk (l % 8) ^ swz(row) of that
+  // row.  The swizzle depends only on j % 2.  A rows past the live rows (Mv)
+  // are clamped; N % BN == 0 keeps B tiles whole.
   const int lrow = 64 * wave + (lane >> 3);
-  int off[2];
+  const int brow = (BN / 4) * wave + (lane >> 3);
+  int boff[2];
 #pragma unroll
-  for (int e = 0; e < 2; ++e) off[e] = lrow * K + (((lane & 7) ^ swz(lrow + 8 * e)) << 3);
+  for (int e = 0; e < 2; ++e) boff[e] = brow * K + (((lane & 7) ^ swz(brow + 8 * e)) << 3);
   const size_t stride8 = (size_t)8 * K;
   const bf16_t* b_src = Bw + (size_t)n0 * K;
   const int a_win = wave * A_IN * 512, b_win = wave * B_IN * 512;
@@ -558,7 +564,7 @@ gemm_bf16_w4_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw,
               As + (kt & 1) * BM * BK + a_win + j * 512);
   };
   auto dma_b = [&](int kt, int j) {
-    lds_dma16(b_src + kt * BK + j * stride8 + off[j & 1], Bs + (kt % NSB) * BN * BK + b_win + j * 512);
+    lds_dma16(b_src + kt * BK + j * stride8 + boff[j & 1], Bs + (kt % NSB) * BN * BK + b_win + j * 512);
   };
   auto frag = [&](bf16x8& f, const bf16_t* base, int row, int kc) {
     f = *reinterpret_cast<const bf16x8*>(base + row * BK + ((kc ^ swz(row)) << 3));
@@ -607,9 +613,12 @@ gemm_bf16_w4_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw,
       constexpr int S = decltype(s_)::value, c = S & 1;
       auto chunk = [&](auto q_) {
         constexpr int Q = decltype(q_)::value;
+        constexpr int HB = B_IN / 2, b0 = Q * HB / 4, b1 = (Q + 1) * HB / 4;
         if constexpr (S == 0 && X) dma_a(kt + 1, A_IN / 2 + Q);
-        if constexpr (S == 1 && Y) dma_b(kt + 2, Q);
-        if constexpr (S == 2 && Y) dma_b(kt + 2, B_IN / 2 + Q);
+        if constexpr (S == 1 && Y)
+          for (int j = b0; j < b1; ++j) dma_b(kt + 2, j);
+        if constexpr (S == 2 && Y)
+          for (int j = b0; j < b1; ++j) dma_b(kt + 2, HB + j);
         if constexpr (S == 3 && Y) dma_a(kt + 2, Q);
         // the next step's first MFMAs need A fragment 0 and every B fragment
         if constexpr (Q == 0) {
@@ -625,7 +634,7 @@ gemm_bf16_w4_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw,
           acc[Q][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[c][Q], fb[c][j], acc[Q][j], 0, 0, 0);
         __builtin_amdgcn_sched_barrier(0);
       };
-      static_assert(TM == 4 && A_IN == 8 && B_IN == 8, "four chunks per k step");
+      static_assert(TM == 4 && A_IN == 8, "four chunks per k step");
       chunk(std::integral_constant<int, 0>{});
       chunk(std::integral_constant<int, 1>{});
       chunk(std::integral_constant<int, 2>{});
@@ -663,11 +672,11 @@ gemm_bf16_w4_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw,
     epilogue_w<BM, BN, EPI, WM, WN>(acc, m0, n0, wm, wn, lane, Mv, N, ea);
 }
 
-template <int EPI>
+template <int EPI, int BN>
 void launch_w4(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int K,
                const int* M_dev, const EpiArgs& ea) {
-  const int n_tm = ceil_div(M, 256), n_tn = ceil_div(N, 256);
-  gemm_bf16_w4_kernel<EPI><<<dim3(n_tm * n_tn), dim3(256), 0, st>>>(A, B, M, N, K, M_dev, ea, n_tm, n_tn);
+  const int n_tm = ceil_div(M, 256), n_tn = N / BN;
+  gemm_bf16_w4_kernel<EPI, BN><<<dim3(n_tm * n_tn), dim3(256), 0, st>>>(A, B, M, N, K, M_dev, ea, n_tm, n_tn);
   DLMC_HIP(hipGetLastError());
 }
 
@@ -679,14 +688,15 @@ void launch_epi(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, 
   DLMC_HIP(hipGetLastError());
 }
 
+template <int BN>
 void launch_256(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int K,
                 const int* M_dev, EpiKind epi, const EpiArgs& ea) {
   switch (epi) {
-    case EPI_STORE_F32: launch_w4<EPI_STORE_F32>(st, A, B, M, N, K, M_dev, ea); break;
-    case EPI_RESIDUAL: launch_w4<EPI_RESIDUAL>(st, A, B, M, N, K, M_dev, ea); break;
-    case EPI_GELU: launch_w4<EPI_GELU>(st, A, B, M, N, K, M_dev, ea); break;
-    case EPI_QKV_ROPE: launch_w4<EPI_QKV_ROPE>(st, A, B, M, N, K, M_dev, ea); break;
-    case EPI_SWIGLU: launch_w4<EPI_SWIGLU>(st, A, B, M, N, K, M_dev, ea); break;
+    case EPI_STORE_F32: launch_w4<EPI_STORE_F32, BN>(st, A, B, M, N, K, M_dev, ea); break;
+    case EPI_RESIDUAL: launch_w4<EPI_RESIDUAL, BN>(st, A, B, M, N, K, M_dev, ea); break;
+    case EPI_GELU: launch_w4<EPI_GELU, BN>(st, A, B, M, N, K, M_dev, ea); break;
+    case EPI_QKV_ROPE: launch_w4<EPI_QKV_ROPE, BN>(st, A, B, M, N, K, M_dev, ea); break;
+    case EPI_SWIGLU: launch_w4<EPI_SWIGLU, BN>(st, A, B, M, N, K, M_dev, ea); break;
   }
 }
 
@@ -722,24 +732,25 @@ void gemm_bf16(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, i
   DLMC_CHECK(!paired || N % 128 == 0, DLMC_E_INVAL, "paired epilogue needs N % 128 == 0");
   DLMC_CHECK(epi != EPI_QKV_ROPE || (ea.d % 128 == 0 && (ea.dh == 64 || ea.dh == 128)),
              DLMC_E_INVAL, "QKV epilogue needs d % 128 == 0 and head dim 64 or 128");
-  // Tile choice (never changes the result), from measurements at M = 2048
-  // with the weights streamed from HBM as in a layer loop:
-  //  - LM head (fp32 store): the 4-wave 256 x 256 kernel when enough rows
-  //    are live;
-  //  - at least three 256 x 256 tiles per CU (the SwiGLU FFN-in GEMM): the
-  //    4-wave 256 x 256 kernel;
-  //  - otherwise 4-wave 128 x 128 (two blocks per CU).
-  const int live = rows_hint >= 0 ? std::min(rows_hint, M) : M;
-  if (epi == EPI_STORE_F32) {
-    if (N % 256 == 0 && live >= 512)
-      launch_256(st, A, B, M, N, K, M_dev, epi, ea);
-    else
-      launch<128, 128>(st, A, B, M, N, K, M_dev, epi, ea);
-  } else if (N % 256 == 0 && (long)ceil_div(live, 256) * (N / 256) >= 3 * 256) {
-    launch_256(st, A, B, M, N, K, M_dev, epi, ea);
-  } else {
+  // Tile choice (never changes the result).  Estimated time is the flops
+  // over (kernel rate x share of computed rows that are live x share of the
+  // tile slots of the last wave of tiles that are filled); the rates are
+  // those measured at M = 2048 with the weights streamed from HBM, as in a
+  // layer loop: 256 x 256 1.23, 256 x 128 1.10, 128 x 128 0.92 PFLOP/s.
+  const int live = std::max(1, rows_hint >= 0 ? std::min(rows_hint, M) : M);
+  auto score = [&](int bm, int bn, long slots, double rate) {
+    const long tm = ceil_div(live, bm), tiles = tm * ceil_div(N, bn);
+    return rate * live / ((double)tm * bm) * tiles / ((double)ceil_div(tiles, slots) * slots);
+  };
+  const double s256 = N % 256 == 0 ? score(256, 256, 256, 1.23) : 0.0;
+  const double s2x1 = N % 128 == 0 ? score(256, 128, 256, 1.10) : 0.0;
+  const double s128 = score(128, 128, 512, 0.92);
+  if (s256 >= s2x1 && s256 >= s128)
+    launch_256<256>(st, A, B, M, N, K, M_dev, epi, ea);
+  else if (s2x1 >= s128)
+    launch_256<128>(st, A, B, M, N, K, M_dev, epi, ea);
+  else
     launch<128, 128>(st, A, B, M, N, K, M_dev, epi, ea);
-  }
 }
 
 }  // namespace dlmc

@@ -110,6 +110,25 @@ def test_logits_bf16_256_tile_ragged_rows():
     check_logits(sh, 2, 256, 0.6, 2e-2, seed=1)
 
 
+@pytest.mark.parametrize("kw", [dict(ffn="swiglu", norm="rmsnorm"), dict(ffn="gelu", norm="layernorm")])
+@pytest.mark.parametrize("B,T", [(1, 300), (2, 256)])
+def test_logits_bf16_256x128_tiles(kw, B, T):
+    """At 300 or 512 rows, d_model 512, FFN 1024 and vocabulary 384, the tile
+    choice puts QKV (rotary epilogue), O-proj and FFN-out (residual), FFN-in
+    (SwiGLU or GELU) and the LM head (fp32 store) on the 4-wave 256 x 128
+    kernel; 300 rows leave its second row tile ragged."""
+    sh = shape(d_model=512, n_heads=4, d_ffn=1024, n_layers=1, vocab=384, **kw)
+    check_logits(sh, B, T, 0.6, 2e-2)
+
+
+def test_logits_bf16_256x256_tiles_head_dim_64():
+    """The small model's layer shape (d_model 768, 12 heads of 64, GELU FFN
+    3072) at 4 x 1024 rows: QKV and FFN-in take the 4-wave 256 x 256 kernel,
+    with the rotary pairs of 64-wide heads inside its 128-column wave tiles."""
+    sh = shape(d_model=768, n_heads=12, d_ffn=3072, n_layers=1, vocab=384)
+    check_logits(sh, 4, 1024, 0.6, 2e-2)
+
+
 def test_logits_bf16_small_config():
     sh = wl.WORKLOADS["small"].model
     check_logits(sh, 1, 1024, 0.7, 2e-2)
