@@ -208,8 +208,10 @@ def main():
     enc.step()
     prof_all = model.profile_read()
     dom = max(gemm_stages, key=lambda s: prof_all[s][0])
-    # the timed passes carry events around the dominant stage and the LM head only
-    model.profile(True, stages=None if args.profile_all else sorted({dom, "head"}))
+    # the timed passes carry events around the dominant stage (in one layer per
+    # pass, rotating through the layers) and the LM head only
+    model.profile(True, stages=None if args.profile_all else sorted({dom, "head"}),
+                  one_layer=not args.profile_all)
     torch.cuda.synchronize()
     c0 = enc.coded
     t0 = time.perf_counter()

@@ -26,6 +26,7 @@ DTYPE = {"f32": 0, "bf16": 1}
 FLAG_CRC = 1
 STAGES = ["embed", "norm", "qkv", "attn", "oproj", "ffn_in", "ffn_out", "head", "entropy",
           "select", "cdf", "reveal", "compact"]
+PROFILE_ONE_LAYER = 1 << 31  # DLMC_PROFILE_ONE_LAYER
 
 
 class LibraryMissing(RuntimeError):
@@ -270,9 +271,11 @@ class Model:
         self._trace_cb = TRACE_FN(cb)
         _check(lib().dlmc_set_trace(self.handle, self._trace_cb, None))
 
-    def profile(self, on: bool = True, stages: Optional[Sequence[str]] = None):
+    def profile(self, on: bool = True, stages: Optional[Sequence[str]] = None,
+                one_layer: bool = False):
         """Enable (all stages, or the named ones) / disable per-stage event
-        timing; every call resets the counters."""
+        timing; every call resets the counters.  one_layer: time the per-layer
+        stages in one layer per forward pass (rotating), not in every layer."""
         if not on:
             mask = 0
         elif stages is None:
@@ -281,6 +284,8 @@ class Model:
             mask = 0
             for name in stages:
                 mask |= 1 << STAGES.index(name)
+        if on and one_layer:
+            mask |= PROFILE_ONE_LAYER
         _check(lib().dlmc_profile_enable(self.handle, mask))
 
     def profile_read(self) -> dict:

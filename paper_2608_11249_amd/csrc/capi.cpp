@@ -297,6 +297,8 @@ dlmc_status dlmc_profile_enable(dlmc_model* m, uint32_t stage_mask) {
     use(m);
     m->prof_reset();
     m->prof = stage_mask & DLMC_PROFILE_ALL;
+    m->prof_one_layer = (stage_mask & DLMC_PROFILE_ONE_LAYER) != 0;
+    m->prof_fwd = 0;
   });
 }
 

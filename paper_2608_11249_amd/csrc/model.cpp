@@ -77,8 +77,11 @@ hipEvent_t dlmc_model::prof_event() {
     prof_pool.pop_back();
     return e;
   }
+  // timing only: the stream is synchronised before the elapsed times are
+  // read, so the events need no system-scope fence (whose L2 writeback would
+  // add several microseconds around each timed launch)
   hipEvent_t e;
-  DLMC_HIP(hipEventCreate(&e));
+  DLMC_HIP(hipEventCreateWithFlags(&e, hipEventDisableSystemFence));
   return e;
 }
 
@@ -282,6 +285,10 @@ void dlmc_model::forward(const int32_t* st_dev, int B, int T, float* logits_out,
   hipStream_t s = stream;
   const double Md = M, dd = d, es = (double)esz;
   const double head_rows = rows_hint >= 0 ? (double)rows_hint : Md;
+  // the one layer whose stages are timed (DLMC_PROFILE_ONE_LAYER), else -1
+  const int timed_layer =
+      prof && prof_one_layer ? (int)(prof_fwd++ % (uint64_t)layers.size()) : -1;
+  prof_gated = false;
 
   {
     StageTimer t(this, DLMC_STAGE_EMBED, Md * dd * (es + 4.0));
@@ -322,6 +329,7 @@ void dlmc_model::forward(const int32_t* st_dev, int B, int T, float* logits_out,
   };
   int layer_index = 0;
   for (const Layer& w : layers) {
+    prof_gated = timed_layer >= 0 && layer_index != timed_layer;
     {
       StageTimer t(this, DLMC_STAGE_NORM, norm_bytes);
       norm_rows(s, x, h, cfg.dtype, M, d, cfg.norm_kind, cfg.norm_eps, nullptr, nullptr);
@@ -392,6 +400,7 @@ void dlmc_model::forward(const int32_t* st_dev, int B, int T, float* logits_out,
     }
     ++layer_index;
   }
+  prof_gated = false;
   if (attn_maps) return;  // context passes need no head
   // masked (or given) rows only: compaction, final norm gathered, LM head
   if (!rows_given) {

@@ -61,7 +61,10 @@ struct dlmc_model {
     hipEvent_t a, b;
     double work;
   };
-  uint32_t prof = 0;  // bit s set: stage s is timed
+  uint32_t prof = 0;            // bit s set: stage s is timed
+  bool prof_one_layer = false;  // per-layer stages timed in one layer per forward
+  uint64_t prof_fwd = 0;        // forwards since profiling was enabled
+  bool prof_gated = false;      // inside a layer that is not timed
   std::vector<ProfRec> prof_recs;
   std::vector<hipEvent_t> prof_pool;
   double prof_ms[DLMC_N_STAGES] = {}, prof_work[DLMC_N_STAGES] = {};
@@ -101,7 +104,7 @@ struct StageTimer {
   double work;
   hipEvent_t a = nullptr;
   StageTimer(dlmc_model* m_, int stage_, double work_) : m(m_), stage(stage_), work(work_) {
-    if (m->prof & (1u << stage_)) {
+    if ((m->prof & (1u << stage_)) && !m->prof_gated) {
       a = m->prof_event();
       DLMC_HIP(hipEventRecord(a, m->stream));
     }

@@ -300,4 +300,10 @@ def test_stage_profile_mask():
         p = m.profile_read()
         assert all(p[s][1] > 0 for s in ("qkv", "attn", "oproj", "ffn_in", "ffn_out", "head", "cdf"))
         assert p["cdf"][2] == 8 * (8.0 * sh.vocab + 4.0)
+        # one layer per forward: one FFN-in launch per pass, the head as usual
+        m.profile(True, stages=["ffn_in", "head"], one_layer=True)
+        for _ in range(3):
+            enc.step()
+        p = m.profile_read()
+        assert p["ffn_in"][1] == 3 and p["head"][1] == 3 and p["qkv"][1] == 0
         m.profile(False)
