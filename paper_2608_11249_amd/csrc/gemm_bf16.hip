@@ -20,6 +20,7 @@
 #include "kernels.h"
 
 #include <type_traits>
+#include <utility>
 
 namespace dlmc {
 namespace {
@@ -343,6 +344,59 @@ __device__ __forceinline__ void epilogue_staged(f32x16 (&acc)[WM / 32][WN / 32],
   }
 }
 
+// fp32 store or residual update of a tile whose staging buffer would not fit
+// in LDS (256 x 256): the same two phases as epilogue_staged, once per
+// 128-row half -- the waves holding the half park it in LDS, then all threads
+// store it (or add it to the residual rows) as float4s.
+template <int EPI, int BM, int BN, int WM, int WN, int NT>
+__device__ __forceinline__ void epilogue_store_halves(f32x16 (&acc)[WM / 32][WN / 32], bf16_t* smem,
+                                                      int m0, int n0, int wm, int wn, int tid,
+                                                      int Mv, int N, const EpiArgs& ea) {
+  static_assert(BM == 2 * WM, "two wave rows");
+  static_assert(EPI == EPI_STORE_F32 || EPI == EPI_RESIDUAL, "fp32 epilogues");
+  constexpr int TM = WM / 32, TN = WN / 32, PF = BN + 8;
+  constexpr int CPR4 = BN / 4, IT4 = WM * CPR4 / NT;
+  static_assert(WM * CPR4 % NT == 0, "fp32 chunks must split evenly over the threads");
+  const int lane = tid & 63, lr = lane & 31, lg = lane >> 5;
+  float* sf = reinterpret_cast<float*>(smem);
+  const bool vec4 = (ea.ldo & 3) == 0;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    if (wm == h) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            sf[(i * 32 + (r >> 2) * 8 + lg * 4 + (r & 3)) * PF + wn * WN + j * 32 + lr] = acc[i][j][r];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int it = 0; it < IT4; ++it) {
+      const int qi = tid + it * NT, row = qi / CPR4, c = (qi % CPR4) * 4;
+      const int grow = m0 + h * WM + row, gcol = n0 + c;
+      if (grow >= Mv) continue;
+      float* dst = (float*)ea.out + (size_t)grow * ea.ldo + gcol;
+      const float* src = sf + row * PF + c;
+      if (gcol + 4 <= N && vec4) {
+        float4 v = *reinterpret_cast<const float4*>(src);
+        if constexpr (EPI == EPI_RESIDUAL) {
+          const float4 o = *reinterpret_cast<const float4*>(dst);
+          v.x = o.x + v.x; v.y = o.y + v.y; v.z = o.z + v.z; v.w = o.w + v.w;
+        }
+        *reinterpret_cast<float4*>(dst) = v;
+      } else {
+        for (int e = 0; e < 4 && gcol + e < N; ++e) {
+          if constexpr (EPI == EPI_RESIDUAL) dst[e] += src[e];
+          else dst[e] = src[e];
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
 // 16-byte direct global -> LDS load (global_load_lds_dwordx4).  `lds` must be
 // wave-uniform: lane l writes lds + 16 l bytes.  The builtin exists only for
 // the device target, so the host pass sees an empty body.
@@ -496,20 +550,25 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, in
 // into LDS, not the MFMAs, are what limits those), and one block per CU
 // covers the narrower GEMMs in whole waves of tiles.
 //
-// LDS stages: A (activation) tile k sits in stage k % 2, B (weight) tile k in
-// stage k % 3 (160 KB in all at BN = 256).  One barrier per k-tile, between k steps 2 and
-// 3: before it each wave has waited for its own direct loads of tile k + 1 and
-// for its fragment reads of tile k; after it, tile k's stages are free, so
-// the loads of tile k + 2 (A and B) go into them while step 3 runs.  A tile
-// k + 1 is thus issued half under step 3 of k-tile k - 1 and half under step 0
-// of k-tile k, B tile k + 2 under steps 1 and 2 of k-tile k, so the weight
-// tile has about two k-tiles to arrive from HBM.
+// LDS stages: A (activation) tile k sits in stage k % NSA, B (weight) tile k
+// in stage k % NSB (NSA = 2, NSB = 3 at BN = 256; 3 and 4 at BN = 128; 160 KB
+// either way).  One barrier per k-tile, between k steps 2 and 3: before it
+// each wave has waited for its own direct loads of tile k + 1 and for its
+// fragment reads of tile k; after it, tile k's stages are free.  The loads
+// into those stages -- A tile k + NSA, B tile k + NSB, together "window k",
+// the operand with fewer stages first -- are spread over the next four k
+// steps (step 3 of k-tile k, steps 0-2 of k-tile k + 1), so a tile is issued
+// NS - 1 k-tiles, less a step or two, before it is read.  Loads arrive from
+// L2 or HBM at a latency of about a k-tile, and more stages hide more of it.
 //
 // Each k step runs as four chunks in a fixed order, split by scheduling
-// barriers: the direct loads due (at most one of A, B_IN / 8 of B), the next
-// step's fragment reads (the first two chunks), BN / 64 MFMAs.  The direct
-// loads of a k-tile are thus spread evenly over it; issued in bursts they back
-// up the load path and hold up the MFMAs behind them.
+// barriers: the direct loads due (NL / 16 of a window's NL loads), the next
+// step's fragment reads (the first two chunks), BN / 64 MFMAs.  Spread evenly,
+// the direct loads do not back up the load path and hold up the MFMAs behind
+// them, as they do when issued in bursts.
+//
+// The last max(NSA, NSB) k-tiles are peeled: loads past the last k-tile are
+// dropped at compile time, so the main loop has no branches.
 //
 // Numerics: each accumulator takes the k steps of each k-tile in order, as in
 // gemm_bf16_kernel, so the results are identical to the other kernel's.
@@ -523,14 +582,46 @@ __device__ __forceinline__ void block_barrier() {
   __builtin_amdgcn_sched_barrier(0);
 }
 
-template <int EPI, int BN>
+// s_waitcnt immediate: vmcnt(n) with lgkmcnt(0)
+constexpr int waitcnt_vm(int n) { return 0x0070 | (n & 15) | ((n >> 4) << 14); }
+
+template <int B0, typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, B0 + I>{}), ...);
+}
+// f(integral_constant<B0>) ... f(integral_constant<B1 - 1>)
+template <int B0, int B1, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl<B0>(f, std::make_integer_sequence<int, (B1 > B0 ? B1 - B0 : 0)>{});
+}
+
+// Loads of a window: I < N1 are those of the operand with fewer stages.
+// Stage count of load I, and the number of prologue loads (windows -NSM ..
+// -2, tiles >= 0) issued after the last load of tile 0.
+template <int NSA, int NSB, int N1>
+constexpr int w4_ns_of(int i) {
+  return ((i < N1) == (NSA <= NSB)) ? NSA : NSB;
+}
+template <int NSA, int NSB, int N1, int NL>
+constexpr int w4_prologue_after_tile0() {
+  constexpr int NSM = NSA > NSB ? NSA : NSB;
+  int after = 0;
+  for (int w = -NSM; w <= -2; ++w)
+    for (int i = 0; i < NL; ++i) {
+      const int tile = w + w4_ns_of<NSA, NSB, N1>(i);
+      if (tile >= 0) after = tile == 0 ? 0 : after + 1;
+    }
+  return after;
+}
+
+template <int EPI, int BN, int NSA, int NSB>
 __global__ void __launch_bounds__(256)
 gemm_bf16_w4_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, int M, int N,
                     int K, const int* __restrict__ M_dev, EpiArgs ea, int n_tm, int n_tn) {
   static_assert(BN == 256 || BN == 128, "256 x 256 or 256 x 128 tiles");
-  constexpr int BM = 256, WM = 128, WN = BN / 2, TM = WM / 32, TN = WN / 32, NSB = 3;
+  constexpr int BM = 256, WM = 128, WN = BN / 2, TM = WM / 32, TN = WN / 32;
   constexpr int A_IN = BM / 32, B_IN = BN / 32;  // 1 KB direct loads per wave per k-tile
-  using SE = StagedEpi<BM, BN, EPI, (2 * BM + NSB * BN) * BK * 2, 1>;
+  using SE = StagedEpi<BM, BN, EPI, (NSA * BM + NSB * BN) * BK * 2, 1>;
   __shared__ __attribute__((aligned(16))) bf16_t smem[SE::smem_elems];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -542,9 +633,10 @@ gemm_bf16_w4_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw,
   tile_coords(n_tm, n_tn, tm, tn);
   const int m0 = tm * BM, n0 = tn * BN;
   if (m0 >= Mv) return;
+  const int nk = K / BK;
 
   bf16_t* As = smem;
-  bf16_t* Bs = smem + 2 * BM * BK;
+  bf16_t* Bs = smem + NSA * BM * BK;
   // direct loads: window j of wave w fills A tile rows 64 w + 8 j .. + 7 (1 KB)
   // or B tile rows (BN / 4) w + 8 j .. + 7; lane l fills row 8 j + l / 8 of the
   // wave's range, 16-byte slot l % 8, with chunk (l % 8) ^ swz(row) of that
@@ -561,13 +653,26 @@ gemm_bf16_w4_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw,
   auto dma_a = [&](int kt, int j) {
     const int chunk = ((lane & 7) ^ swz(lrow + 8 * (j & 1))) << 3;
     lds_dma16(A + (min(m0 + lrow + 8 * j, Mv - 1) * K + kt * BK + chunk),
-              As + (kt & 1) * BM * BK + a_win + j * 512);
+              As + (kt % NSA) * BM * BK + a_win + j * 512);
   };
   auto dma_b = [&](int kt, int j) {
     lds_dma16(b_src + kt * BK + j * stride8 + boff[j & 1], Bs + (kt % NSB) * BN * BK + b_win + j * 512);
   };
   auto frag = [&](bf16x8& f, const bf16_t* base, int row, int kc) {
     f = *reinterpret_cast<const bf16x8*>(base + row * BK + ((kc ^ swz(row)) << 3));
+  };
+  // load I of window w: A tile w + NSA, B tile w + NSB, fewer stages first
+  constexpr bool A_FIRST = NSA <= NSB;
+  constexpr int NL = A_IN + B_IN, N1 = A_FIRST ? A_IN : B_IN;
+  constexpr int NSM = NSA > NSB ? NSA : NSB, NSMIN = NSA < NSB ? NSA : NSB;
+  auto load = [&](int w, auto i_) {
+    constexpr int I = decltype(i_)::value;
+    constexpr bool IS_A = (I < N1) == A_FIRST;
+    constexpr int J = I < N1 ? I : I - N1;
+    if constexpr (IS_A)
+      dma_a(w + NSA, J);
+    else
+      dma_b(w + NSB, J);
   };
 
   f32x16 acc[TM][TN];
@@ -578,48 +683,53 @@ gemm_bf16_w4_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw,
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  const int nk = K / BK;
-  // s_waitcnt encodings: vmcnt(0) / vmcnt(B_IN), each with lgkmcnt(0)
-  constexpr int WAIT_ALL = 0x0070, WAIT_B_AHEAD = 0x0070 | B_IN;
-  static_assert(B_IN < 16, "vmcnt field");
-#pragma unroll
-  for (int j = 0; j < A_IN; ++j) dma_a(0, j);
-#pragma unroll
-  for (int j = 0; j < B_IN; ++j) dma_b(0, j);
-  if (nk > 1) {
-#pragma unroll
-    for (int j = 0; j < B_IN; ++j) dma_b(1, j);
-    __builtin_amdgcn_s_waitcnt(WAIT_B_AHEAD);
-  } else {
-    __builtin_amdgcn_s_waitcnt(WAIT_ALL);
-  }
+  // Wait counts.  At the end of k-tile t the windows up to t - 1 have been
+  // issued; YOUNGER of their loads follow the last load of tile t + 1.
+  constexpr int YOUNGER = (NSA == NSB ? 0 : (A_FIRST ? B_IN : A_IN)) + (NSMIN - 2) * NL;
+  // prologue: windows -NSM .. -2, tiles >= 0; PROL loads follow the last
+  // load of tile 0
+  constexpr int PROL = w4_prologue_after_tile0<NSA, NSB, N1, NL>();
+  static_assert(YOUNGER < 64 && PROL < 64, "vmcnt field");
+  static_for<-NSM, -1>([&](auto w_) {
+    constexpr int W = decltype(w_)::value;
+    static_for<0, NL>([&](auto i_) {
+      constexpr int TILE = W + w4_ns_of<NSA, NSB, N1>(decltype(i_)::value);
+      if constexpr (TILE >= 0)
+        if (TILE < nk) load(W, i_);
+    });
+  });
+  if (nk >= NSM - 1)
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(PROL));
+  else
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
   block_barrier();
-  if (nk > 1) {
-#pragma unroll
-    for (int j = 0; j < A_IN / 2; ++j) dma_a(1, j);
-  }
+  // the first quarter of window -1 (what step 3 of k-tile -1 would issue)
+  static_for<0, NL / 4>([&](auto i_) {
+    if (w4_ns_of<NSA, NSB, N1>(decltype(i_)::value) - 1 < nk) load(-1, i_);
+  });
   bf16x8 fa[2][TM], fb[2][TN];
   load_frags<TM>(fa[0], As, wm * WM, lr, lg);
   load_frags<TN>(fb[0], Bs, wn * WN, lr, lg);
 
-  // one k-tile.  X: A tile kt + 1 exists (its second half is issued in step
-  // 0); Y: tile kt + 2 exists (B in steps 1 and 2, the first half of A in
-  // step 3).
-  auto trip = [&](int kt, auto x_, auto y_) {
-    constexpr bool X = decltype(x_)::value, Y = decltype(y_)::value;
+  // One k-tile.  Steps 0-2 issue the last three quarters of window kt - 1,
+  // step 3 (after the barrier) the first quarter of window kt.  R < 0: a
+  // main-loop k-tile, every load exists; R >= 0: k-tile nk - NSM + R, loads
+  // of tiles >= nk dropped.
+  auto trip = [&](int kt, auto r_) {
+    constexpr int R = decltype(r_)::value;
     // k step S: MFMAs on fragment set S % 2 while the other set is read from
     // (an, bn) at 16-byte chunk kc
     auto step = [&](auto s_, const bf16_t* an, const bf16_t* bn, int kc) {
       constexpr int S = decltype(s_)::value, c = S & 1;
+      constexpr int W_OFF = S == 3 ? 0 : -1;  // window kt + W_OFF
       auto chunk = [&](auto q_) {
         constexpr int Q = decltype(q_)::value;
-        constexpr int HB = B_IN / 2, b0 = Q * HB / 4, b1 = (Q + 1) * HB / 4;
-        if constexpr (S == 0 && X) dma_a(kt + 1, A_IN / 2 + Q);
-        if constexpr (S == 1 && Y)
-          for (int j = b0; j < b1; ++j) dma_b(kt + 2, j);
-        if constexpr (S == 2 && Y)
-          for (int j = b0; j < b1; ++j) dma_b(kt + 2, HB + j);
-        if constexpr (S == 3 && Y) dma_a(kt + 2, Q);
+        constexpr int SLOT = ((S + 1) & 3) * 4 + Q;  // slots 0-3: step 3; 4-15: steps 0-2
+        static_for<SLOT * NL / 16, (SLOT + 1) * NL / 16>([&](auto i_) {
+          // tile - nk of this load in k-tile nk - NSM + R
+          constexpr int PAST = W_OFF + w4_ns_of<NSA, NSB, N1>(decltype(i_)::value) - NSM + R;
+          if constexpr (R < 0 || PAST < 0) load(kt + W_OFF, i_);
+        });
         // the next step's first MFMAs need A fragment 0 and every B fragment
         if constexpr (Q == 0) {
 #pragma unroll
@@ -634,40 +744,35 @@ gemm_bf16_w4_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw,
           acc[Q][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[c][Q], fb[c][j], acc[Q][j], 0, 0, 0);
         __builtin_amdgcn_sched_barrier(0);
       };
-      static_assert(TM == 4 && A_IN == 8, "four chunks per k step");
-      chunk(std::integral_constant<int, 0>{});
-      chunk(std::integral_constant<int, 1>{});
-      chunk(std::integral_constant<int, 2>{});
-      chunk(std::integral_constant<int, 3>{});
+      static_assert(TM == 4, "four chunks per k step");
+      static_for<0, 4>(chunk);
     };
-    const bf16_t* as = As + (kt & 1) * BM * BK;
+    const bf16_t* as = As + (kt % NSA) * BM * BK;
     const bf16_t* bs = Bs + (kt % NSB) * BN * BK;
     step(std::integral_constant<int, 0>{}, as, bs, 2 + lg);
     step(std::integral_constant<int, 1>{}, as, bs, 4 + lg);
     step(std::integral_constant<int, 2>{}, as, bs, 6 + lg);
-    // A tile kt + 1 (and B tile kt + 1, issued earlier) have landed; only B
-    // tile kt + 2 may still be in flight
-    if constexpr (Y)
-      __builtin_amdgcn_s_waitcnt(WAIT_B_AHEAD);
+    // tile kt + 1 has landed and this wave's reads of tile kt are done; once
+    // loads have been dropped, fewer than YOUNGER follow it: wait for all
+    if constexpr (R <= 0)
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(YOUNGER));
     else
-      __builtin_amdgcn_s_waitcnt(WAIT_ALL);
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
     block_barrier();
-    step(std::integral_constant<int, 3>{}, As + ((kt + 1) & 1) * BM * BK,
+    step(std::integral_constant<int, 3>{}, As + ((kt + 1) % NSA) * BM * BK,
          Bs + ((kt + 1) % NSB) * BN * BK, lg);
   };
-  using T_ = std::true_type;
-  using F_ = std::false_type;
-  int kt = 0;
-  for (; kt + 2 < nk; ++kt) trip(kt, T_{}, T_{});
-  if (kt + 2 == nk) {
-    trip(kt, T_{}, F_{});
-    ++kt;
-  }
-  trip(kt, F_{}, F_{});  // its fragment reads past the last k-tile are unused
-  __builtin_amdgcn_s_waitcnt(WAIT_ALL);
+  for (int kt = 0; kt < nk - NSM; ++kt) trip(kt, std::integral_constant<int, -1>{});
+  static_for<0, NSM>([&](auto r_) {
+    constexpr int R = decltype(r_)::value;
+    if (nk - NSM + R >= 0) trip(nk - NSM + R, r_);  // its fragment reads past the last k-tile are unused
+  });
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
   block_barrier();
   if constexpr (SE::enabled)
     epilogue_staged<BM, BN, EPI, WM, WN, 256>(acc, smem, m0, n0, wm, wn, tid, Mv, N, ea);
+  else if constexpr ((EPI == EPI_STORE_F32 || EPI == EPI_RESIDUAL) && WM * (BN + 8) * 4 <= 160 * 1024)
+    epilogue_store_halves<EPI, BM, BN, WM, WN, 256>(acc, smem, m0, n0, wm, wn, tid, Mv, N, ea);
   else
     epilogue_w<BM, BN, EPI, WM, WN>(acc, m0, n0, wm, wn, lane, Mv, N, ea);
 }
@@ -675,8 +780,11 @@ gemm_bf16_w4_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw,
 template <int EPI, int BN>
 void launch_w4(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int K,
                const int* M_dev, const EpiArgs& ea) {
+  // stage counts: 160 KB of LDS either way
+  constexpr int NSA = BN == 256 ? 2 : 3, NSB = BN == 256 ? 3 : 4;
   const int n_tm = ceil_div(M, 256), n_tn = N / BN;
-  gemm_bf16_w4_kernel<EPI, BN><<<dim3(n_tm * n_tn), dim3(256), 0, st>>>(A, B, M, N, K, M_dev, ea, n_tm, n_tn);
+  gemm_bf16_w4_kernel<EPI, BN, NSA, NSB>
+      <<<dim3(n_tm * n_tn), dim3(256), 0, st>>>(A, B, M, N, K, M_dev, ea, n_tm, n_tn);
   DLMC_HIP(hipGetLastError());
 }
 
