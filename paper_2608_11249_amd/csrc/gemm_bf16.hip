@@ -34,22 +34,30 @@ constexpr int BK = 64;
 // distinct 16-byte bank slots (8 for even rows, 8 for odd rows).
 __device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
 
-// Tile of block `bid`.  Hardware block ids go round robin over the 8 XCDs;
-// the remap gives each XCD a contiguous range of logical tiles, and the
-// logical order walks groups of 8 m-tiles (m fastest inside a group), so the
-// blocks resident on one XCD at a time cover about 8 x 8 tiles and share their
-// operand panels through that XCD's L2.
-__device__ __forceinline__ void tile_coords(int n_tm, int n_tn, int& tm, int& tn) {
+// Tile of this block among the tiles with live rows (the first Mv of M).
+// Hardware block ids go round robin over the 8 XCDs; the remap gives each XCD
+// a contiguous range of the live tiles (launches use a multiple of 8 blocks,
+// at least one per tile), and the logical order walks groups of 8 m-tiles (m
+// fastest inside a group), so the blocks resident on one XCD at a time cover
+// about 8 x 8 tiles and share their operand panels through that XCD's L2.
+// Spreading the live tiles, not all M rows' tiles, keeps every XCD busy when
+// few rows are live.  Returns false for a block without a tile.
+__device__ __forceinline__ bool tile_coords(int n_tm, int n_tn, int bm, int Mv, int& tm, int& tn) {
+  const int tm_live = min(n_tm, (Mv + bm - 1) / bm);
+  const int n_live = tm_live * n_tn;
+  const int nb = (n_live + 7) & ~7;
   int l = blockIdx.x;
-  const int nb = gridDim.x;
-  if ((nb & 7) == 0) l = (l & 7) * (nb >> 3) + (l >> 3);
+  if (l >= nb) return false;
+  l = (l & 7) * (nb >> 3) + (l >> 3);
+  if (l >= n_live) return false;
   constexpr int G = 8;
   const int per_group = G * n_tn;
   const int g = l / per_group, first = g * G;
-  const int gsize = min(n_tm - first, G);
+  const int gsize = min(tm_live - first, G);
   const int r = l - g * per_group;
   tm = first + r % gsize;
   tn = r / gsize;
+  return true;
 }
 
 __device__ __forceinline__ float gelu_erf(float v) {
@@ -448,9 +456,8 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, in
   const int lr = lane & 31, lg = lane >> 5;
   const int Mv = M_dev ? min(*M_dev, M) : M;
   int tm, tn;
-  tile_coords(n_tm, n_tn, tm, tn);
+  if (!tile_coords(n_tm, n_tn, BM, Mv, tm, tn)) return;
   const int m0 = tm * BM, n0 = tn * BN;
-  if (m0 >= Mv) return;
 
   bf16_t* As = smem;
   bf16_t* Bs = smem + 2 * BM * BK;
@@ -630,9 +637,8 @@ gemm_bf16_w4_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw,
   const int lr = lane & 31, lg = lane >> 5;
   const int Mv = M_dev ? min(*M_dev, M) : M;
   int tm, tn;
-  tile_coords(n_tm, n_tn, tm, tn);
+  if (!tile_coords(n_tm, n_tn, BM, Mv, tm, tn)) return;
   const int m0 = tm * BM, n0 = tn * BN;
-  if (m0 >= Mv) return;
   const int nk = K / BK;
 
   bf16_t* As = smem;
@@ -784,7 +790,7 @@ void launch_w4(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, i
   constexpr int NSA = BN == 256 ? 2 : 3, NSB = BN == 256 ? 3 : 4;
   const int n_tm = ceil_div(M, 256), n_tn = N / BN;
   gemm_bf16_w4_kernel<EPI, BN, NSA, NSB>
-      <<<dim3(n_tm * n_tn), dim3(256), 0, st>>>(A, B, M, N, K, M_dev, ea, n_tm, n_tn);
+      <<<dim3(round_up(n_tm * n_tn, 8)), dim3(256), 0, st>>>(A, B, M, N, K, M_dev, ea, n_tm, n_tn);
   DLMC_HIP(hipGetLastError());
 }
 
@@ -792,7 +798,7 @@ template <int BM, int BN, int EPI>
 void launch_epi(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int K,
                 const int* M_dev, const EpiArgs& ea) {
   const int n_tm = ceil_div(M, BM), n_tn = ceil_div(N, BN);
-  gemm_bf16_kernel<BM, BN, EPI><<<dim3(n_tm * n_tn), dim3(256), 0, st>>>(A, B, M, N, K, M_dev, ea, n_tm, n_tn);
+  gemm_bf16_kernel<BM, BN, EPI><<<dim3(round_up(n_tm * n_tn, 8)), dim3(256), 0, st>>>(A, B, M, N, K, M_dev, ea, n_tm, n_tn);
   DLMC_HIP(hipGetLastError());
 }
 
