@@ -16,7 +16,9 @@
 // LDS with direct loads (global_load_lds_dwordx4) into a double buffer, so no
 // registers stage them and two waves fit per SIMD.  Key tiles are visited in
 // a fixed order, so results do not depend on the launch shape or on other
-// chunks.
+// chunks.  A block holds QB = 128 or 256 queries (4 or 8 waves, two waves per
+// SIMD either way); with 256 every K / V tile moved into LDS serves twice as
+// many queries, which halves the tile traffic per CU.
 #include <type_traits>
 
 #include "kernels.h"
@@ -24,8 +26,7 @@
 namespace dlmc {
 namespace {
 
-constexpr int KT = 64;   // keys per tile
-constexpr int QB = 128;  // queries per block (4 waves x 32)
+constexpr int KT = 64;  // keys per tile
 
 // LDS row i of a K tile holds key sigma(i) of the tile (an involution)
 __device__ __forceinline__ int sigma(int i) { return (i & ~12) | ((i & 4) << 1) | ((i & 8) >> 1); }
@@ -52,16 +53,18 @@ __device__ __forceinline__ void lds_dma16(const bf16_t* g, bf16_t* lds) {
 #endif
 }
 
-template <int DH>
-__global__ void __launch_bounds__(256, 2)
+template <int DH, int QB>
+__global__ void __launch_bounds__(2 * QB, 256 / QB)
 attn_bf16_kernel(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kg,
                  const bf16_t* __restrict__ Vt, bf16_t* __restrict__ O, int H, int T, int Tp,
                  float scale_log2) {
+  constexpr int NWV = QB / 32;       // waves per block (32 queries each)
   constexpr int NS = DH / 16;        // k steps of S^T
   constexpr int RB = DH * 2;         // bytes per K row
   constexpr int KRW = 1024 / RB;     // K rows per 1 KB load window
-  constexpr int KW = KT / KRW / 4;   // K windows per wave
-  constexpr int VW = DH / 8 / 4;     // V^T windows (8 rows of 128 B) per wave
+  constexpr int KW = KT / KRW / NWV; // K windows per wave
+  constexpr int VW = DH / 8 / NWV;   // V^T windows (8 rows of 128 B) per wave
+  static_assert(KW >= 1 && VW >= 1 && KW * KRW * NWV == KT && VW * 8 * NWV == DH, "tile split");
   constexpr int NV = DH / 32 * 4;    // PV MFMAs per tile
   __shared__ __attribute__((aligned(16))) bf16_t Ks[2][KT * DH];
   __shared__ __attribute__((aligned(16))) bf16_t Vs[2][DH * KT];
@@ -313,15 +316,24 @@ attn_f32_kernel(const float* __restrict__ Q, const float* __restrict__ Kg,
 void attention_bf16(hipStream_t st, const bf16_t* q, const bf16_t* k, const bf16_t* vt,
                     bf16_t* out, int B, int H, int T, int Tp, int dh) {
   if (B <= 0 || T <= 0) return;
-  DLMC_CHECK(Tp % QB == 0 && Tp >= T, DLMC_E_INVAL, "attention: padded length must be a multiple of 128");
-  dim3 grid(ceil_div(T, QB), H, B), block(256);
+  DLMC_CHECK(Tp % 128 == 0 && Tp >= T, DLMC_E_INVAL, "attention: padded length must be a multiple of 128");
+  DLMC_CHECK(dh == 128 || dh == 64, DLMC_E_INVAL, "bf16 attention supports head dims 64 and 128");
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)dh);
+  // 256-query blocks (half the K / V traffic per CU) when the padded rows
+  // cover them and there is at least one block per CU; else 128
+  const bool wide = Tp % 256 == 0 && (long)(Tp / 256) * H * B >= 256;
+  auto run = [&](auto dh_c, auto qb_c) {
+    constexpr int DH = decltype(dh_c)::value, QB = decltype(qb_c)::value;
+    dim3 grid(ceil_div(T, QB), H, B), block(2 * QB);
+    attn_bf16_kernel<DH, QB><<<grid, block, 0, st>>>(q, k, vt, out, H, T, Tp, scale_log2);
+  };
+  using I64 = std::integral_constant<int, 64>;
+  using I128 = std::integral_constant<int, 128>;
+  using I256 = std::integral_constant<int, 256>;
   if (dh == 128) {
-    attn_bf16_kernel<128><<<grid, block, 0, st>>>(q, k, vt, out, H, T, Tp, scale_log2);
-  } else if (dh == 64) {
-    attn_bf16_kernel<64><<<grid, block, 0, st>>>(q, k, vt, out, H, T, Tp, scale_log2);
+    if (wide) run(I128{}, I256{}); else run(I128{}, I128{});
   } else {
-    throw Error(DLMC_E_INVAL, "bf16 attention supports head dims 64 and 128");
+    if (wide) run(I64{}, I256{}); else run(I64{}, I128{});
   }
   DLMC_HIP(hipGetLastError());
 }

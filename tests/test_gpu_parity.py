@@ -129,6 +129,15 @@ def test_logits_bf16_256x256_tiles_head_dim_64():
     check_logits(sh, 4, 1024, 0.6, 2e-2)
 
 
+@pytest.mark.parametrize("d_model,n_heads,B,T", [(2048, 32, 1, 2000), (1024, 8, 4, 1999)])
+def test_logits_attention_256_query_blocks(d_model, n_heads, B, T):
+    """With at least one 256-query block per CU ((Tp / 256) x heads x batch >=
+    256) attention runs 8-wave blocks of 256 queries; a ragged T leaves
+    queries and keys past T in the last block (head dims 64 and 128)."""
+    sh = shape(d_model=d_model, n_heads=n_heads, d_ffn=512, n_layers=1, vocab=384)
+    check_logits(sh, B, T, 0.6, 2e-2)
+
+
 def test_logits_bf16_small_config():
     sh = wl.WORKLOADS["small"].model
     check_logits(sh, 1, 1024, 0.7, 2e-2)
