@@ -167,7 +167,9 @@ def copy_calibration(nbytes):
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    # 128 passes = one chunk's worth at k = 16 (2048 / 16): with the warmup
+    # passes, the timed passes see every masked-row count of a chunk once
+    ap.add_argument("--steps", type=int, default=128)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="8b",
                     choices=["tiny", "small", "8b", "8b-throughput", "8b-long"])
