@@ -63,7 +63,13 @@ __device__ __forceinline__ bool tile_coords(int n_tm, int n_tn, int bm, int Mv, 
 __device__ __forceinline__ float gelu_erf(float v) {
   return 0.5f * v * (1.0f + erff(v * 0.70710678118654752440f));
 }
-__device__ __forceinline__ float silu(float v) { return v / (1.0f + expf(-v)); }
+// SiLU from the hardware 2^x and reciprocal (v_exp_f32, v_rcp_f32): a few
+// ulps of fp32, and the product with the up projection is rounded to bf16
+// right after.  Large negative v: 2^x overflows to +inf and the result is -0.
+__device__ __forceinline__ float silu(float v) {
+  const float e = __builtin_amdgcn_exp2f(-v * 1.4426950408889634f);
+  return v * __builtin_amdgcn_rcpf(1.0f + e);
+}
 
 // acc[i][j][r] holds C[row][col] with row = i*32 + (r/4)*8 + lg*4 + r%4 and
 // col = j*32 + lr inside the wave tile of wave (wm, wn).
