@@ -60,8 +60,19 @@ __device__ __forceinline__ bool tile_coords(int n_tm, int n_tn, int bm, int Mv, 
   return true;
 }
 
+// GELU, 0.5 v (1 + erf(v / sqrt 2)), with erfc(x) for x = |v| / sqrt 2 from the
+// rational approximation of Abramowitz and Stegun, formula 7.1.26 (absolute
+// error at most 1.5e-7), on the hardware 2^x and reciprocal; the result is
+// rounded to bf16 right after.
 __device__ __forceinline__ float gelu_erf(float v) {
-  return 0.5f * v * (1.0f + erff(v * 0.70710678118654752440f));
+  const float x = fabsf(v) * 0.70710678118654752440f;
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, x, 1.0f));
+  const float poly =
+      t * fmaf(t, fmaf(t, fmaf(t, fmaf(t, 1.061405429f, -1.453152027f), 1.421413741f), -0.284496736f),
+               0.254829592f);
+  const float erfc_x = poly * __builtin_amdgcn_exp2f(-x * x * 1.4426950408889634f);
+  // v >= 0: 0.5 v (2 - erfc); v < 0: 0.5 v erfc
+  return v >= 0.0f ? v * (1.0f - 0.5f * erfc_x) : 0.5f * v * erfc_x;
 }
 // SiLU from the hardware 2^x and reciprocal (v_exp_f32, v_rcp_f32): a few
 // ulps of fp32, and the product with the up projection is rounded to bf16
