@@ -71,12 +71,20 @@ attn_bf16_kernel(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kg,
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 31, lg = lane >> 5;
-  const int h = blockIdx.y, b = blockIdx.z;
+  // 1-D grid of (query block, head, batch).  Hardware block ids go round
+  // robin over the 8 XCDs; the remap gives each XCD a contiguous range of
+  // logical blocks, so the query blocks of a head run on one XCD and share
+  // that head's K / V tiles through its L2.
+  const int nqb = (T + QB - 1) / QB;
+  const int nb = gridDim.x;
+  int bid = blockIdx.x;
+  if ((nb & 7) == 0) bid = (bid & 7) * (nb >> 3) + (bid >> 3);
+  const int qblk = bid % nqb, h = (bid / nqb) % H, b = bid / (nqb * H);
   const size_t bh = (size_t)b * H + h;
   const bf16_t* Qp = Q + bh * Tp * DH;
   const bf16_t* Kp = Kg + bh * Tp * DH;
   const bf16_t* Vp = Vt + bh * DH * Tp;
-  const int q0 = blockIdx.x * QB + wave * 32;
+  const int q0 = qblk * QB + wave * 32;
 
   // B operand of S^T = K Q^T: lane holds Q[q0 + lr][16 s + 8 lg .. + 7]
   bf16x8 qf[NS];
@@ -324,7 +332,7 @@ void attention_bf16(hipStream_t st, const bf16_t* q, const bf16_t* k, const bf16
   const bool wide = Tp % 256 == 0 && (long)(Tp / 256) * H * B >= 256;
   auto run = [&](auto dh_c, auto qb_c) {
     constexpr int DH = decltype(dh_c)::value, QB = decltype(qb_c)::value;
-    dim3 grid(ceil_div(T, QB), H, B), block(2 * QB);
+    dim3 grid(ceil_div(T, QB) * H * B), block(2 * QB);
     attn_bf16_kernel<DH, QB><<<grid, block, 0, st>>>(q, k, vt, out, H, T, Tp, scale_log2);
   };
   using I64 = std::integral_constant<int, 64>;
