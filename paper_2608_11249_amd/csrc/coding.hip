@@ -63,11 +63,18 @@ struct Stat {
   float m, Z, A;
 };
 
+// e^t for t <= 0 on the hardware 2^x (a few ulps of fp32, far inside the
+// entropy tolerance; the kernel is bound by this arithmetic, not by memory,
+// with the accurate expf)
+__device__ __forceinline__ float exp_neg(float t) {
+  return __builtin_amdgcn_exp2f(t * 1.4426950408889634f);
+}
+
 __device__ __forceinline__ Stat merge(Stat x, Stat y) {
   if (y.Z == 0.0f) return x;
   if (x.Z == 0.0f) return y;
   const float m = fmaxf(x.m, y.m);
-  const float cx = expf(x.m - m), cy = expf(y.m - m);
+  const float cx = exp_neg(x.m - m), cy = exp_neg(y.m - m);
   Stat r;
   r.m = m;
   r.Z = cx * x.Z + cy * y.Z;
@@ -79,7 +86,7 @@ __device__ __forceinline__ void add4(Stat& s, f32x4 v) {
   const float mx = fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w));
   if (mx > s.m) {
     if (s.Z > 0.0f) {
-      const float c = expf(s.m - mx);
+      const float c = exp_neg(s.m - mx);
       s.A = c * (s.A + (s.m - mx) * s.Z);
       s.Z = c * s.Z;
     }
@@ -89,7 +96,7 @@ __device__ __forceinline__ void add4(Stat& s, f32x4 v) {
   for (int e = 0; e < 4; ++e) {
     if (v[e] == -INFINITY) continue;  // padding of a ragged row
     const float t = v[e] - s.m;
-    const float p = expf(t);
+    const float p = exp_neg(t);
     s.Z += p;
     s.A += p * t;
   }
