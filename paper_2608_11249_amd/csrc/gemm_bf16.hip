@@ -247,23 +247,41 @@ __device__ __forceinline__ void epilogue_staged(f32x16 (&acc)[WM / 32][WN / 32],
     const int d = ea.d, dh = ea.dh, T = ea.T, half = dh / 2;
     const int which = n0 / d;
     if (which < 2) {
+      constexpr int NP = TN / 2;  // (lo, hi) pairs of 32-column blocks per wave tile row
+      int hb[NP], dlo[NP];        // local column of the head's first dim; dim of lo
 #pragma unroll
-      for (int j = 0; j < TN; j += 2) {
-        const int lc0 = wc0 + j * 32;               // local column of the (lo, hi) pair
+      for (int p = 0; p < NP; ++p) {
+        const int lc0 = wc0 + 2 * p * 32;
         const int in_head = (n0 + lc0) % d % dh;
-        const int hb = lc0 - in_head;               // local column of the head's first dim
-        const int dlo = ((in_head / 32) >> 1) * 32 + lr;
+        hb[p] = lc0 - in_head;
+        dlo[p] = ((in_head / 32) >> 1) * 32 + lr;
+      }
+      // the cos / sin gathers of a 32-row block are all issued before the
+      // first is used: issued one at a time, each would wait out an L2 round
+      // trip, and those waits made this epilogue cost a third of the tile's
+      // main loop
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
+      for (int i = 0; i < TM; ++i) {
+        float cv[NP][16], sv[NP][16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = wr0 + i * 32 + (r >> 2) * 8 + lg * 4 + (r & 3);
+          const int t = min(m0 + row, Mv - 1) % T;
+#pragma unroll
+          for (int p = 0; p < NP; ++p) {
+            cv[p][r] = ea.rope_cos[t * half + dlo[p]];
+            sv[p][r] = ea.rope_sin[t * half + dlo[p]];
+          }
+        }
+#pragma unroll
+        for (int p = 0; p < NP; ++p)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int row = wr0 + i * 32 + (r >> 2) * 8 + lg * 4 + (r & 3);
-            const int grow = min(m0 + row, Mv - 1);
-            const int t = grow % T;
-            const float lo = acc[i][j][r], hi = acc[i][j + 1][r];
-            const float c = ea.rope_cos[t * half + dlo], s = ea.rope_sin[t * half + dlo];
-            smem[row * SE::PB + hb + dlo] = f32_to_bf16(lo * c - hi * s);
-            smem[row * SE::PB + hb + dlo + half] = f32_to_bf16(hi * c + lo * s);
+            const float lo = acc[i][2 * p][r], hi = acc[i][2 * p + 1][r];
+            const float c = cv[p][r], s = sv[p][r];
+            smem[row * SE::PB + hb[p] + dlo[p]] = f32_to_bf16(lo * c - hi * s);
+            smem[row * SE::PB + hb[p] + dlo[p] + half] = f32_to_bf16(hi * c + lo * s);
           }
       }
     } else {
