@@ -659,7 +659,8 @@ constexpr int w4_prologue_after_tile0() {
 template <int EPI, int BN, int NSA, int NSB>
 __global__ void __launch_bounds__(256)
 gemm_bf16_w4_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, int M, int N,
-                    int K, const int* __restrict__ M_dev, EpiArgs ea, int n_tm, int n_tn) {
+                    int K, const int* __restrict__ M_dev, EpiArgs ea, int n_tm, int n_tn,
+                    int tn_off) {
   static_assert(BN == 256 || BN == 128, "256 x 256 or 256 x 128 tiles");
   constexpr int BM = 256, WM = 128, WN = BN / 2, TM = WM / 32, TN = WN / 32;
   constexpr int A_IN = BM / 32, B_IN = BN / 32;  // 1 KB direct loads per wave per k-tile
@@ -673,7 +674,7 @@ gemm_bf16_w4_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw,
   const int Mv = M_dev ? min(*M_dev, M) : M;
   int tm, tn;
   if (!tile_coords(n_tm, n_tn, BM, Mv, tm, tn)) return;
-  const int m0 = tm * BM, n0 = tn * BN;
+  const int m0 = tm * BM, n0 = (tn + tn_off) * BN;  // the launch covers column tiles tn_off ..
   const int nk = K / BK;
 
   bf16_t* As = smem;
@@ -818,14 +819,16 @@ gemm_bf16_w4_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw,
     epilogue_w<BM, BN, EPI, WM, WN>(acc, m0, n0, wm, wn, lane, Mv, N, ea);
 }
 
+// columns [c0, c1) of C, both multiples of BN
 template <int EPI, int BN>
 void launch_w4(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int K,
-               const int* M_dev, const EpiArgs& ea) {
+               const int* M_dev, const EpiArgs& ea, int c0, int c1) {
   // stage counts: 160 KB of LDS either way
   constexpr int NSA = BN == 256 ? 2 : 3, NSB = BN == 256 ? 3 : 4;
-  const int n_tm = ceil_div(M, 256), n_tn = N / BN;
-  gemm_bf16_w4_kernel<EPI, BN, NSA, NSB>
-      <<<dim3(round_up(n_tm * n_tn, 8)), dim3(256), 0, st>>>(A, B, M, N, K, M_dev, ea, n_tm, n_tn);
+  const int n_tm = ceil_div(M, 256), n_tn = (c1 - c0) / BN;
+  if (n_tn <= 0) return;
+  gemm_bf16_w4_kernel<EPI, BN, NSA, NSB><<<dim3(round_up(n_tm * n_tn, 8)), dim3(256), 0, st>>>(
+      A, B, M, N, K, M_dev, ea, n_tm, n_tn, c0 / BN);
   DLMC_HIP(hipGetLastError());
 }
 
@@ -839,13 +842,13 @@ void launch_epi(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, 
 
 template <int BN>
 void launch_256(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int K,
-                const int* M_dev, EpiKind epi, const EpiArgs& ea) {
+                const int* M_dev, EpiKind epi, const EpiArgs& ea, int c0, int c1) {
   switch (epi) {
-    case EPI_STORE_F32: launch_w4<EPI_STORE_F32, BN>(st, A, B, M, N, K, M_dev, ea); break;
-    case EPI_RESIDUAL: launch_w4<EPI_RESIDUAL, BN>(st, A, B, M, N, K, M_dev, ea); break;
-    case EPI_GELU: launch_w4<EPI_GELU, BN>(st, A, B, M, N, K, M_dev, ea); break;
-    case EPI_QKV_ROPE: launch_w4<EPI_QKV_ROPE, BN>(st, A, B, M, N, K, M_dev, ea); break;
-    case EPI_SWIGLU: launch_w4<EPI_SWIGLU, BN>(st, A, B, M, N, K, M_dev, ea); break;
+    case EPI_STORE_F32: launch_w4<EPI_STORE_F32, BN>(st, A, B, M, N, K, M_dev, ea, c0, c1); break;
+    case EPI_RESIDUAL: launch_w4<EPI_RESIDUAL, BN>(st, A, B, M, N, K, M_dev, ea, c0, c1); break;
+    case EPI_GELU: launch_w4<EPI_GELU, BN>(st, A, B, M, N, K, M_dev, ea, c0, c1); break;
+    case EPI_QKV_ROPE: launch_w4<EPI_QKV_ROPE, BN>(st, A, B, M, N, K, M_dev, ea, c0, c1); break;
+    case EPI_SWIGLU: launch_w4<EPI_SWIGLU, BN>(st, A, B, M, N, K, M_dev, ea, c0, c1); break;
   }
 }
 
@@ -881,25 +884,53 @@ void gemm_bf16(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, i
   DLMC_CHECK(!paired || N % 128 == 0, DLMC_E_INVAL, "paired epilogue needs N % 128 == 0");
   DLMC_CHECK(epi != EPI_QKV_ROPE || (ea.d % 128 == 0 && (ea.dh == 64 || ea.dh == 128)),
              DLMC_E_INVAL, "QKV epilogue needs d % 128 == 0 and head dim 64 or 128");
-  // Tile choice (never changes the result).  Estimated time is the flops
-  // over (kernel rate x share of computed rows that are live x share of the
-  // tile slots of the last wave of tiles that are filled); the rates are
-  // those measured at M = 2048 with the weights streamed from HBM, as in a
-  // layer loop: 256 x 256 1.23, 256 x 128 1.10, 128 x 128 0.92 PFLOP/s.
+  // Tile choice (never changes the result).  Estimated time of an option:
+  // its flops over (kernel rate x share of computed rows that are live x
+  // share of the tile slots of its last wave of tiles that are filled), with
+  // the rates measured at M = 2048 with the weights streamed from HBM, as in
+  // a layer loop: 256 x 256 1.23, 256 x 128 1.10, 128 x 128 0.92 PFLOP/s.
+  // The 4-wave kernel may also split the columns: 256 x 256 tiles on the
+  // first c1, 256 x 128 tiles on the rest (two launches), so that each
+  // launch fills whole waves of tiles (QKV at M = 2048: Q and K on 256
+  // tiles, V on 256 more, instead of three waves of 256 x 128 tiles).
   const int live = std::max(1, rows_hint >= 0 ? std::min(rows_hint, M) : M);
-  auto score = [&](int bm, int bn, long slots, double rate) {
-    const long tm = ceil_div(live, bm), tiles = tm * ceil_div(N, bn);
-    return rate * live / ((double)tm * bm) * tiles / ((double)ceil_div(tiles, slots) * slots);
+  auto t_of = [&](int bm, int bn, long slots, double rate, long cols) -> double {
+    if (cols <= 0) return 0.0;
+    const long tm = ceil_div(live, bm), tiles = tm * (long)ceil_div((int)cols, bn);
+    const double eff = (double)tiles / ((double)((tiles + slots - 1) / slots) * slots);
+    return (double)cols / (rate * live / ((double)tm * bm) * eff);
   };
-  const double s256 = N % 256 == 0 ? score(256, 256, 256, 1.23) : 0.0;
-  const double s2x1 = N % 128 == 0 ? score(256, 128, 256, 1.10) : 0.0;
-  const double s128 = score(128, 128, 512, 0.92);
-  if (s256 >= s2x1 && s256 >= s128)
-    launch_256<256>(st, A, B, M, N, K, M_dev, epi, ea);
-  else if (s2x1 >= s128)
-    launch_256<128>(st, A, B, M, N, K, M_dev, epi, ea);
-  else
+  const double t128 = t_of(128, 128, 512, 0.92, N);
+  double t4 = 1e300;
+  int split = -1;  // columns on 256 x 256 tiles
+  // a QKV tile must lie inside one of Q, K, V: 256-wide tiles need d % 256 == 0
+  const bool wide_ok = epi != EPI_QKV_ROPE || ea.d % 256 == 0;
+  if (N % 128 == 0) {
+    auto t_split = [&](int c1) {
+      return t_of(256, 256, 256, 1.23, c1) + t_of(256, 128, 256, 1.10, N - c1);
+    };
+    // one launch (all 256 x 128, or all 256 x 256), then a two-launch split
+    // if it is more than 3% faster (the second launch has a cost of its own)
+    split = 0;
+    t4 = t_split(0);
+    if (wide_ok && N % 256 == 0 && t_split(N) < t4 * (1.0 - 1e-9)) {
+      split = N;
+      t4 = t_split(N);
+    }
+    for (int c1 = 256; wide_ok && c1 < N; c1 += 256) {
+      const double t = t_split(c1);
+      if (t < t4 * 0.97) {
+        t4 = t;
+        split = c1;
+      }
+    }
+  }
+  if (split >= 0 && t4 <= t128) {
+    launch_256<256>(st, A, B, M, N, K, M_dev, epi, ea, 0, split);
+    launch_256<128>(st, A, B, M, N, K, M_dev, epi, ea, split, N);
+  } else {
     launch<128, 128>(st, A, B, M, N, K, M_dev, epi, ea);
+  }
 }
 
 }  // namespace dlmc

@@ -129,6 +129,22 @@ def test_logits_bf16_256x256_tiles_head_dim_64():
     check_logits(sh, 4, 1024, 0.6, 2e-2)
 
 
+def test_logits_bf16_column_split_tiles():
+    """GELU FFN of 4352 at 4 x 1024 rows: FFN-in splits its columns between a
+    256 x 256 launch (columns 0..2303, 9 x 16 tiles) and a 256 x 128 launch
+    (the other 2048, 16 x 16 tiles), each filling whole waves of tiles."""
+    sh = shape(d_model=256, n_heads=4, d_ffn=4352, n_layers=1, vocab=384)
+    check_logits(sh, 4, 1024, 0.6, 2e-2)
+
+
+def test_logits_qkv_no_wide_tiles_across_q_k_v():
+    """d_model 1408 (11 heads of 128) at 4 x 1024 rows: a column split of QKV
+    would put a 256-wide tile across the Q / K boundary (column 1408), so QKV
+    stays on 256 x 128 tiles, each inside one of Q, K and V."""
+    sh = shape(d_model=1408, n_heads=11, d_ffn=512, n_layers=1, vocab=384)
+    check_logits(sh, 4, 1024, 0.6, 2e-2)
+
+
 @pytest.mark.parametrize("d_model,n_heads,B,T", [(2048, 32, 1, 2000), (1024, 8, 4, 1999)])
 def test_logits_attention_256_query_blocks(d_model, n_heads, B, T):
     """With at least one 256-query block per CU ((Tp / 256) x heads x batch >=
