@@ -95,9 +95,10 @@ def cpu_baseline(w, layers_timed=1, vocab_sample=4096):
 
 
 def roundtrip_leg(model, w):
-    """One batch of whole chunks encoded into a container, then decoded, each
-    timed end to end (host tokens in, host bytes out): decode throughput and
-    bits per input byte, which the timed encode passes cannot give."""
+    """One batch of whole chunks encoded into a container (one streaming
+    encoder step per pass), then decoded, each timed end to end (host tokens
+    in, host bytes out): decode throughput, bits per input byte and the pass
+    count, which the timed encode passes cannot give."""
     import numpy as np
     import torch
 
@@ -106,10 +107,21 @@ def roundtrip_leg(model, w):
     toks = wl.make_tokens(w, cd.batch * cd.chunk_len)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    data = model.encode(toks, cd)
+    enc = model.encoder(cd, toks)
+    passes = 0
+    try:
+        while not enc.step():
+            passes += 1
+        passes += 1
+        data = enc.finish()
+    finally:
+        enc.close()
     t1 = time.perf_counter()
+    print(f"roundtrip: encoded {len(toks)} tokens in {passes} passes, {t1 - t0:.1f} s",
+          file=sys.stderr, flush=True)
     back = model.decode(data)
     t2 = time.perf_counter()
+    print(f"roundtrip: decoded in {t2 - t1:.1f} s", file=sys.stderr, flush=True)
     if not np.array_equal(back, toks):
         raise RuntimeError("round trip mismatch")
     nb = len(toks) * w.token_bytes
@@ -117,6 +129,9 @@ def roundtrip_leg(model, w):
         "tokens": int(len(toks)),
         "container_bytes": len(data),
         "bits_per_input_byte": round(8.0 * len(data) / nb, 4),
+        # passes of the batch: every chunk starts at pass 0, so this is the
+        # largest pass count of its chunks (all equal under a fixed k)
+        "passes": passes,
         "encode_s": round(t1 - t0, 3),
         "decode_s": round(t2 - t1, 3),
         "encode_bytes_per_s": round(nb / (t1 - t0), 1),
