@@ -200,8 +200,8 @@ def main():
         copy_calibration(args.copy_calibration)
         return
     if args.gpus != 1:
-        print("bench.py runs on one GPU only: the compression path shards by independent "
-              "chunks (see DESIGN.md); --gpus must be 1", file=sys.stderr)
+        print("bench.py runs on one GPU only: chunks are independent, so several GPUs "
+              "would each encode their own range of chunks; --gpus must be 1", file=sys.stderr)
         sys.exit(2)
 
     import torch
