@@ -129,12 +129,14 @@ def test_logits_bf16_256x256_tiles_head_dim_64():
     check_logits(sh, 4, 1024, 0.6, 2e-2)
 
 
-def test_logits_bf16_column_split_tiles():
-    """GELU FFN of 4352 at 4 x 1024 rows: FFN-in splits its columns between a
-    256 x 256 launch (columns 0..2303, 9 x 16 tiles) and a 256 x 128 launch
-    (the other 2048, 16 x 16 tiles), each filling whole waves of tiles."""
+@pytest.mark.parametrize("B,T", [(4, 1024), (3, 1300)])
+def test_logits_bf16_column_split_tiles(B, T):
+    """GELU FFN of 4352 at 4096 or 3900 rows: FFN-in splits its columns
+    between a 256 x 256 launch (columns 0..2303, 9 x 16 tiles) and a 256 x 128
+    launch (the other 2048, 16 x 16 tiles), each filling whole waves of tiles;
+    at 3900 rows the last row tile of both launches holds 60 live rows."""
     sh = shape(d_model=256, n_heads=4, d_ffn=4352, n_layers=1, vocab=384)
-    check_logits(sh, 4, 1024, 0.6, 2e-2)
+    check_logits(sh, B, T, 0.6, 2e-2)
 
 
 def test_logits_qkv_no_wide_tiles_across_q_k_v():
@@ -169,6 +171,23 @@ def test_logits_batch_invariant():
         for b in (0, 3):
             one, r1 = m.forward_logits(dev_state(st[b:b + 1]))
             sel = (rows >= b * 96) & (rows < (b + 1) * 96)
+            assert np.array_equal(one.cpu().numpy(), lg[sel])
+
+
+def test_logits_batch_invariant_across_tile_choices():
+    """Four chunks of 1024 put FFN-in (4352 columns) on the two-launch column
+    split; one chunk alone puts it on a single launch of other tiles.  Every
+    chunk's logits must still be bit-identical: each output is the same
+    sequential sum over k-tiles whatever tile computes it."""
+    sh = shape(d_model=256, n_heads=4, d_ffn=4352, n_layers=1, vocab=384)
+    st = wl.random_state(11, 4, 1024, sh.vocab, 0.6)
+    with dl.Model(sh, max_chunk=1024, max_batch=4) as m:
+        lg, rows = m.forward_logits(dev_state(st))
+        lg, rows = lg.cpu().numpy(), rows.cpu().numpy()
+        for b in (0, 3):
+            one, r1 = m.forward_logits(dev_state(st[b:b + 1]))
+            sel = (rows >= b * 1024) & (rows < (b + 1) * 1024)
+            assert np.array_equal(r1.cpu().numpy() + b * 1024, rows[sel])
             assert np.array_equal(one.cpu().numpy(), lg[sel])
 
 
