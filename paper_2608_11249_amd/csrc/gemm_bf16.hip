@@ -11,7 +11,8 @@
 //    (128 x 128 tiles, two blocks per CU; small and ragged shapes);
 //  - gemm_bf16_w4_kernel: four waves, one per SIMD, on a 256 x 256 or
 //    256 x 128 tile, A double- and B triple-buffered in LDS (every GEMM of
-//    the 8B-shaped pass).
+//    the 8B-shaped pass); gemm_bf16_w4_split_kernel runs both tile shapes
+//    in one launch, on two column ranges.
 //
 // Numerics: each output element is a sequential sum over k-tiles, each k-tile
 // four MFMA steps in order, independent of the kernel, the tile shape and of
@@ -42,11 +43,11 @@ __device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
 // about 8 x 8 tiles and share their operand panels through that XCD's L2.
 // Spreading the live tiles, not all M rows' tiles, keeps every XCD busy when
 // few rows are live.  Returns false for a block without a tile.
-__device__ __forceinline__ bool tile_coords(int n_tm, int n_tn, int bm, int Mv, int& tm, int& tn) {
+__device__ __forceinline__ bool tile_coords(int bid, int n_tm, int n_tn, int bm, int Mv, int& tm, int& tn) {
   const int tm_live = min(n_tm, (Mv + bm - 1) / bm);
   const int n_live = tm_live * n_tn;
   const int nb = (n_live + 7) & ~7;
-  int l = blockIdx.x;
+  int l = bid;
   if (l >= nb) return false;
   l = (l & 7) * (nb >> 3) + (l >> 3);
   if (l >= n_live) return false;
@@ -491,7 +492,7 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, in
   const int lr = lane & 31, lg = lane >> 5;
   const int Mv = M_dev ? min(*M_dev, M) : M;
   int tm, tn;
-  if (!tile_coords(n_tm, n_tn, BM, Mv, tm, tn)) return;
+  if (!tile_coords(blockIdx.x, n_tm, n_tn, BM, Mv, tm, tn)) return;
   const int m0 = tm * BM, n0 = tn * BN;
 
   bf16_t* As = smem;
@@ -656,16 +657,24 @@ constexpr int w4_prologue_after_tile0() {
   return after;
 }
 
+// LDS elements (bf16) of one 4-wave block: the operand stages, or the staged
+// epilogue's tile where that is larger
 template <int EPI, int BN, int NSA, int NSB>
-__global__ void __launch_bounds__(256)
-gemm_bf16_w4_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, int M, int N,
-                    int K, const int* __restrict__ M_dev, EpiArgs ea, int n_tm, int n_tn,
-                    int tn_off) {
+constexpr int w4_smem_elems() {
+  return StagedEpi<256, BN, EPI, (NSA * 256 + NSB * BN) * BK * 2, 1>::smem_elems;
+}
+
+// One block of the 4-wave kernel: tile number `bid` of a launch over n_tm x
+// n_tn tiles whose columns start at tile tn_off, with `smem` the block's LDS.
+template <int EPI, int BN, int NSA, int NSB>
+__device__ __forceinline__ void w4_tile(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw,
+                                        int M, int N, int K, const int* __restrict__ M_dev,
+                                        const EpiArgs& ea, int n_tm, int n_tn, int tn_off, int bid,
+                                        bf16_t* smem) {
   static_assert(BN == 256 || BN == 128, "256 x 256 or 256 x 128 tiles");
   constexpr int BM = 256, WM = 128, WN = BN / 2, TM = WM / 32, TN = WN / 32;
   constexpr int A_IN = BM / 32, B_IN = BN / 32;  // 1 KB direct loads per wave per k-tile
   using SE = StagedEpi<BM, BN, EPI, (NSA * BM + NSB * BN) * BK * 2, 1>;
-  __shared__ __attribute__((aligned(16))) bf16_t smem[SE::smem_elems];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, kept scalar
@@ -673,7 +682,7 @@ gemm_bf16_w4_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw,
   const int lr = lane & 31, lg = lane >> 5;
   const int Mv = M_dev ? min(*M_dev, M) : M;
   int tm, tn;
-  if (!tile_coords(n_tm, n_tn, BM, Mv, tm, tn)) return;
+  if (!tile_coords(bid, n_tm, n_tn, BM, Mv, tm, tn)) return;
   const int m0 = tm * BM, n0 = (tn + tn_off) * BN;  // the launch covers column tiles tn_off ..
   const int nk = K / BK;
 
@@ -819,6 +828,34 @@ gemm_bf16_w4_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw,
     epilogue_w<BM, BN, EPI, WM, WN>(acc, m0, n0, wm, wn, lane, Mv, N, ea);
 }
 
+template <int EPI, int BN, int NSA, int NSB>
+__global__ void __launch_bounds__(256)
+gemm_bf16_w4_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, int M, int N,
+                    int K, const int* __restrict__ M_dev, EpiArgs ea, int n_tm, int n_tn,
+                    int tn_off) {
+  __shared__ __attribute__((aligned(16))) bf16_t smem[w4_smem_elems<EPI, BN, NSA, NSB>()];
+  w4_tile<EPI, BN, NSA, NSB>(A, Bw, M, N, K, M_dev, ea, n_tm, n_tn, tn_off, blockIdx.x, smem);
+}
+
+// A column split in one launch: blocks [0, nb1) take the 256 x 256 tiles of
+// columns [0, 256 n_tn1), the others the 256 x 128 tiles of the remaining
+// 128 n_tn2 columns.  Blocks start in id order, so the 256 x 128 tiles begin
+// on each CU as soon as its 256 x 256 tile ends; nb1 is a multiple of 8,
+// which keeps each part's XCD mapping.
+template <int EPI>
+__global__ void __launch_bounds__(256)
+gemm_bf16_w4_split_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, int M,
+                          int N, int K, const int* __restrict__ M_dev, EpiArgs ea, int n_tm,
+                          int n_tn1, int n_tn2, int nb1) {
+  constexpr int E1 = w4_smem_elems<EPI, 256, 2, 3>(), E2 = w4_smem_elems<EPI, 128, 3, 4>();
+  __shared__ __attribute__((aligned(16))) bf16_t smem[E1 > E2 ? E1 : E2];
+  if ((int)blockIdx.x < nb1)
+    w4_tile<EPI, 256, 2, 3>(A, Bw, M, N, K, M_dev, ea, n_tm, n_tn1, 0, blockIdx.x, smem);
+  else
+    w4_tile<EPI, 128, 3, 4>(A, Bw, M, N, K, M_dev, ea, n_tm, n_tn2, 2 * n_tn1,
+                            (int)blockIdx.x - nb1, smem);
+}
+
 // columns [c0, c1) of C, both multiples of BN
 template <int EPI, int BN>
 void launch_w4(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int K,
@@ -830,6 +867,28 @@ void launch_w4(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, i
   gemm_bf16_w4_kernel<EPI, BN, NSA, NSB><<<dim3(round_up(n_tm * n_tn, 8)), dim3(256), 0, st>>>(
       A, B, M, N, K, M_dev, ea, n_tm, n_tn, c0 / BN);
   DLMC_HIP(hipGetLastError());
+}
+
+// 256 x 256 tiles on columns [0, c1), 256 x 128 tiles on [c1, N), one launch
+template <int EPI>
+void launch_w4_split(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int K,
+                     const int* M_dev, const EpiArgs& ea, int c1) {
+  const int n_tm = ceil_div(M, 256), n_tn1 = c1 / 256, n_tn2 = (N - c1) / 128;
+  const int nb1 = round_up(n_tm * n_tn1, 8), nb2 = round_up(n_tm * n_tn2, 8);
+  gemm_bf16_w4_split_kernel<EPI><<<dim3(nb1 + nb2), dim3(256), 0, st>>>(
+      A, B, M, N, K, M_dev, ea, n_tm, n_tn1, n_tn2, nb1);
+  DLMC_HIP(hipGetLastError());
+}
+
+void launch_split(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int K,
+                  const int* M_dev, EpiKind epi, const EpiArgs& ea, int c1) {
+  switch (epi) {
+    case EPI_STORE_F32: launch_w4_split<EPI_STORE_F32>(st, A, B, M, N, K, M_dev, ea, c1); break;
+    case EPI_RESIDUAL: launch_w4_split<EPI_RESIDUAL>(st, A, B, M, N, K, M_dev, ea, c1); break;
+    case EPI_GELU: launch_w4_split<EPI_GELU>(st, A, B, M, N, K, M_dev, ea, c1); break;
+    case EPI_QKV_ROPE: launch_w4_split<EPI_QKV_ROPE>(st, A, B, M, N, K, M_dev, ea, c1); break;
+    case EPI_SWIGLU: launch_w4_split<EPI_SWIGLU>(st, A, B, M, N, K, M_dev, ea, c1); break;
+  }
 }
 
 template <int BM, int BN, int EPI>
@@ -890,9 +949,9 @@ void gemm_bf16(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, i
   // the rates measured at M = 2048 with the weights streamed from HBM, as in
   // a layer loop: 256 x 256 1.23, 256 x 128 1.10, 128 x 128 0.92 PFLOP/s.
   // The 4-wave kernel may also split the columns: 256 x 256 tiles on the
-  // first c1, 256 x 128 tiles on the rest (two launches), so that each
-  // launch fills whole waves of tiles (QKV at M = 2048: Q and K on 256
-  // tiles, V on 256 more, instead of three waves of 256 x 128 tiles).
+  // first c1, 256 x 128 tiles on the rest (one launch), so that each part
+  // fills whole waves of tiles (QKV at M = 2048: Q and K on 256 tiles, V on
+  // 256 more, instead of three waves of 256 x 128 tiles).
   const int live = std::max(1, rows_hint >= 0 ? std::min(rows_hint, M) : M);
   auto t_of = [&](int bm, int bn, long slots, double rate, long cols) -> double {
     if (cols <= 0) return 0.0;
@@ -926,8 +985,12 @@ void gemm_bf16(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, i
     }
   }
   if (split >= 0 && t4 <= t128) {
-    launch_256<256>(st, A, B, M, N, K, M_dev, epi, ea, 0, split);
-    launch_256<128>(st, A, B, M, N, K, M_dev, epi, ea, split, N);
+    if (split > 0 && split < N) {
+      launch_split(st, A, B, M, N, K, M_dev, epi, ea, split);
+    } else {
+      launch_256<256>(st, A, B, M, N, K, M_dev, epi, ea, 0, split);
+      launch_256<128>(st, A, B, M, N, K, M_dev, epi, ea, split, N);
+    }
   } else {
     launch<128, 128>(st, A, B, M, N, K, M_dev, epi, ea);
   }
