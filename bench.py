@@ -144,9 +144,21 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ffn_in_gemm_8b_traffic.md")
 GEMM_SOURCE = os.path.join(ROOT, "paper_2608_11249_amd", "csrc", "gemm_bf16.hip")
 
 
-def gemm_source_hash():
+def code_hash(path):
+    """sha256[:16] of a C++ source with its // comments, trailing blanks and
+    empty lines removed: the code the counters were taken on, so that an edit
+    to comments alone keeps a summary valid."""
     import hashlib
-    return hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()[:16]
+    lines = []
+    for line in open(path, encoding="utf-8"):
+        line = line.split("//", 1)[0].rstrip()
+        if line:
+            lines.append(line)
+    return hashlib.sha256("\n".join(lines).encode()).hexdigest()[:16]
+
+
+def gemm_source_hash():
+    return code_hash(GEMM_SOURCE)
 
 
 def measured_traffic():
@@ -159,7 +171,7 @@ def measured_traffic():
         if ": " in line and line.startswith("- "):
             k, v = line[2:].split(": ", 1)
             vals[k.strip()] = v.strip().strip("`")
-    if vals.get("gemm_bf16.hip sha256[:16]") != gemm_source_hash():
+    if vals.get("gemm_bf16.hip code sha256[:16]") != gemm_source_hash():
         return None
     try:
         return float(vals["traffic_bytes_per_launch"])

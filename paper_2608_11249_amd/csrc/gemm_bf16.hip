@@ -259,8 +259,8 @@ __device__ __forceinline__ void epilogue_staged(f32x16 (&acc)[WM / 32][WN / 32],
       }
       // the cos / sin gathers of a 32-row block are all issued before the
       // first is used: issued one at a time, each would wait out an L2 round
-      // trip, and those waits made this epilogue cost a third of the tile's
-      // main loop
+      // trip, and those waits made this epilogue cost more than half as much
+      // as the tile's main loop
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         float cv[NP][16], sv[NP][16];
@@ -968,8 +968,9 @@ void gemm_bf16(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, i
     auto t_split = [&](int c1) {
       return t_of(256, 256, 256, 1.23, c1) + t_of(256, 128, 256, 1.10, N - c1);
     };
-    // one launch (all 256 x 128, or all 256 x 256), then a two-launch split
-    // if it is more than 3% faster (the second launch has a cost of its own)
+    // one tile shape (all 256 x 128, or all 256 x 256), then a split if it
+    // is more than 3% faster (the estimate rounds each part up to whole
+    // waves on its own, a margin for the split's tiles that share a wave)
     split = 0;
     t4 = t_split(0);
     if (wide_ok && N % 256 == 0 && t_split(N) < t4 * (1.0 - 1e-9)) {

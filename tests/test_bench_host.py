@@ -22,7 +22,7 @@ def _summary(path, digest, traffic="6.5000e+08"):
     with open(path, "w") as f:
         f.write("# HBM traffic\n\n")
         f.write(f"- traffic_bytes_per_launch: `{traffic}`\n")
-        f.write(f"- gemm_bf16.hip sha256[:16]: `{digest}`\n")
+        f.write(f"- gemm_bf16.hip code sha256[:16]: `{digest}`\n")
 
 
 def test_measured_traffic_only_for_the_profiled_source(tmp_path, monkeypatch):
@@ -35,6 +35,15 @@ def test_measured_traffic_only_for_the_profiled_source(tmp_path, monkeypatch):
     assert bench.measured_traffic() is None                      # another source
     _summary(path, bench.gemm_source_hash(), traffic="n/a")
     assert bench.measured_traffic() is None                      # unreadable value
+
+
+def test_code_hash_ignores_comments_only(tmp_path):
+    a, b, c = tmp_path / "a.hip", tmp_path / "b.hip", tmp_path / "c.hip"
+    a.write_text("int f() {  // one\n  return 1;\n}\n")
+    b.write_text("// header\n\nint f() {  // two\n  return 1;   \n}\n")
+    c.write_text("int f() {\n  return 2;\n}\n")
+    assert bench.code_hash(a) == bench.code_hash(b)
+    assert bench.code_hash(a) != bench.code_hash(c)
 
 
 def test_needed_tokens_cover_the_timed_passes():
