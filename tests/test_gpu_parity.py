@@ -288,6 +288,22 @@ def test_roundtrip_batch_invariance(dec_batch):
     assert payloads(a) == payloads(b)
 
 
+def test_roundtrip_batch_invariance_8b_layer_shape():
+    """One layer of the 8B shape, two chunks of 2048: with batch 2 (4096 rows)
+    QKV runs on 256 x 256 tiles and O-proj / FFN-out on 256 x 256; with
+    batch 1 (2048 rows) QKV runs the column-split kernel and the residual
+    GEMMs 256 x 128 tiles.  The payloads must still be byte-identical, and
+    the batch-2 container must decode with batch 1."""
+    sh = shape(d_model=4096, n_heads=32, d_ffn=12288, ffn="swiglu", norm="rmsnorm", n_layers=1,
+               vocab=384)
+    cd = codec(2048, k=64, batch=2)
+    toks = wl.markov1_tokens(2 * 2048, sh.vocab, 13)
+    with dl.Model(sh, max_chunk=2048, max_batch=2) as m:
+        a = roundtrip(m, toks, cd, batch_dec=1)
+        b = m.encode(toks, cd, batch=1)
+    assert payloads(a) == payloads(b)
+
+
 @pytest.mark.parametrize("kw,cd,n", [
     (dict(), codec(100, tau=4.0, mmin=1, mmax=8, batch=3), 350),
     (dict(ffn="swiglu", norm="rmsnorm", vocab=70000), codec(128, k=16, P=24, W=64, batch=2), 300),
