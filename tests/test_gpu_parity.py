@@ -304,6 +304,19 @@ def test_roundtrip_batch_invariance_8b_layer_shape():
     assert payloads(a) == payloads(b)
 
 
+def test_roundtrip_batch_invariance_attention_block_size():
+    """One layer of the small model's shape (12 heads of 64), eight chunks of
+    1024: with batch 8 attention runs 256-query blocks ((1024 / 256) x 12 x 8
+    >= 256), with batch 1 128-query blocks.  The payloads must not change."""
+    sh = shape(d_model=768, n_heads=12, d_ffn=3072, n_layers=1, vocab=384)
+    cd = codec(1024, k=64, batch=8)
+    toks = wl.markov1_tokens(8 * 1024, sh.vocab, 14)
+    with dl.Model(sh, max_chunk=1024, max_batch=8) as m:
+        a = roundtrip(m, toks, cd, batch_dec=1)
+        b = m.encode(toks, cd, batch=1)
+    assert payloads(a) == payloads(b)
+
+
 @pytest.mark.parametrize("kw,cd,n", [
     (dict(), codec(100, tau=4.0, mmin=1, mmax=8, batch=3), 350),
     (dict(ffn="swiglu", norm="rmsnorm", vocab=70000), codec(128, k=16, P=24, W=64, batch=2), 300),
