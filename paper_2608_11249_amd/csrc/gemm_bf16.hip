@@ -83,6 +83,16 @@ __device__ __forceinline__ float silu(float v) {
   return v * __builtin_amdgcn_rcpf(1.0f + e);
 }
 
+// Rotary embedding of the pair (lo, hi) = (q_i, q_{i + d_head/2}) at angle
+// (c, s) = (cos, sin): one fused multiply-add each, written out so that every
+// kernel rounds it the same way.
+__device__ __forceinline__ float rot_lo(float lo, float hi, float c, float s) {
+  return fmaf(lo, c, -(hi * s));
+}
+__device__ __forceinline__ float rot_hi(float lo, float hi, float c, float s) {
+  return fmaf(hi, c, lo * s);
+}
+
 // acc[i][j][r] holds C[row][col] with row = i*32 + (r/4)*8 + lg*4 + r%4 and
 // col = j*32 + lr inside the wave tile of wave (wm, wn).
 template <int BM, int BN, int EPI, int WM, int WN>
@@ -111,8 +121,8 @@ __device__ __forceinline__ void epilogue_w(f32x16 (&acc)[WM / 32][WN / 32], int 
             const int dlo = (jb >> 1) * 32 + lr;
             const float c = ea.rope_cos[t * half + dlo], s = ea.rope_sin[t * half + dlo];
             bf16_t* dst = (bf16_t*)(which == 0 ? ea.q : ea.k) + (bh * Tp + t) * dh;
-            dst[dlo] = f32_to_bf16(lo * c - hi * s);
-            dst[dlo + half] = f32_to_bf16(hi * c + lo * s);
+            dst[dlo] = f32_to_bf16(rot_lo(lo, hi, c, s));
+            dst[dlo + half] = f32_to_bf16(rot_hi(lo, hi, c, s));
           } else {
             bf16_t* dst = (bf16_t*)ea.vt + bh * dh * Tp + t;
             const int dim = jb * 32 + lr;
@@ -281,8 +291,8 @@ __device__ __forceinline__ void epilogue_staged(f32x16 (&acc)[WM / 32][WN / 32],
             const int row = wr0 + i * 32 + (r >> 2) * 8 + lg * 4 + (r & 3);
             const float lo = acc[i][2 * p][r], hi = acc[i][2 * p + 1][r];
             const float c = cv[p][r], s = sv[p][r];
-            smem[row * SE::PB + hb[p] + dlo[p]] = f32_to_bf16(lo * c - hi * s);
-            smem[row * SE::PB + hb[p] + dlo[p] + half] = f32_to_bf16(hi * c + lo * s);
+            smem[row * SE::PB + hb[p] + dlo[p]] = f32_to_bf16(rot_lo(lo, hi, c, s));
+            smem[row * SE::PB + hb[p] + dlo[p] + half] = f32_to_bf16(rot_hi(lo, hi, c, s));
           }
       }
     } else {
