@@ -62,14 +62,18 @@ def softmax(s: np.ndarray, axis: int = -1) -> np.ndarray:
 
 def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, want_probs: bool = False):
     """Full (non-causal) softmax attention; q, k, v are [T, H, d_head].  With
-    want_probs also the probabilities [H, Tq, Tk]."""
-    d_head = q.shape[-1]
-    qh = np.ascontiguousarray(q.transpose(1, 0, 2))      # [H, T, dh]
-    kh = np.ascontiguousarray(k.transpose(1, 2, 0))      # [H, dh, T]
-    vh = np.ascontiguousarray(v.transpose(1, 0, 2))      # [H, T, dh]
-    p = softmax((qh @ kh) / math.sqrt(d_head), axis=-1)  # [H, Tq, Tk]
-    o = (p @ vh).transpose(1, 0, 2)
-    return (o, p) if want_probs else o
+    want_probs also the probabilities [H, Tq, Tk].  Heads are independent and
+    are computed one at a time, so a long chunk needs one [T, T] score matrix
+    at a time."""
+    T, H, d_head = q.shape
+    o = np.empty((T, H, d_head), dtype=np.result_type(q, k, v))
+    probs = []
+    for h in range(H):
+        p = softmax((q[:, h, :] @ k[:, h, :].T) / math.sqrt(d_head), axis=-1)   # [Tq, Tk]
+        o[:, h, :] = p @ v[:, h, :]
+        if want_probs:
+            probs.append(p)
+    return (o, np.stack(probs)) if want_probs else o
 
 
 def gelu(x: np.ndarray) -> np.ndarray:
