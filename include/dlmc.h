@@ -162,6 +162,24 @@ dlmc_status dlmc_set_stream(dlmc_model* model, void* hip_stream);
 
 /* ---- compression ------------------------------------------------------- */
 
+/* Container (version 3, little endian).  The header stores the window
+ * length and every schedule parameter, so that the decoder replays the
+ * encoder's decisions from it alone (Implementation Details; the remark
+ * closing Symbol Commitment Schedules):
+ *   0 magic "DLMC", 4 version, 8 header bytes, 12 flags, 16 model hash
+ *   (FNV-1a 64 of the config fields that change results and the seed),
+ *   24 seed, 32 n_tokens, 40 n_chunks, 48 chunk_len, 52 cdf_bits,
+ *   56 coder_bits, 60 m_min, 64 m_max, 68 tau_bits (f32), 72 batch,
+ *   76 schedule, 80 blocks, 84 u1, 88 growth (f64), 96 coder, 100 context,
+ *   104 context_kind, 108 rank_compressor, 112 rank_level, 116 reserved,
+ *   120 numerics id (dlmc_numerics_id), 128 first chunk held, 136 number of
+ *   chunks held (count); then u64 offsets[count + 1] of the held chunks'
+ *   payloads in the payload section, then (DLMC_FLAG_CRC) u32 CRC-32 of each
+ *   held chunk's tokens (as int32), then the payload section.  A chunk's
+ *   payload is its initial context (c u16 positions ascending, then c u32
+ *   symbols) followed by its coder's bytes; the symbol ranking back end
+ *   stores the whole payload section compressed as one block. */
+
 /* Worst-case container size in bytes for n_tokens tokens. */
 dlmc_status dlmc_encode_bound(const dlmc_model* model, const dlmc_codec_params* codec,
                               uint64_t n_tokens, uint64_t* bytes);
@@ -170,8 +188,40 @@ dlmc_status dlmc_encode_bound(const dlmc_model* model, const dlmc_codec_params* 
 dlmc_status dlmc_encode(dlmc_model* model, const dlmc_codec_params* codec,
                         const int32_t* tokens, uint64_t n, uint8_t* out, uint64_t cap,
                         uint64_t* out_len);
-/* Number of tokens a container holds (reads the header only; E_FORMAT). */
+/* Encode only the chunks [first_chunk, first_chunk + n_chunks) of host
+ * tokens[0..n) (chunk i covers tokens [i w, min(n, (i + 1) w)), w =
+ * codec->chunk_len) into a partial container that holds them under their
+ * global indices.  Windows are independent (Implementation Details: non-
+ * overlapping windows can be processed in parallel, e.g. one range per GPU),
+ * so the chunk payloads are byte-identical to those of dlmc_encode of the
+ * whole input.  n_chunks = UINT64_MAX means "to the last chunk"; a range
+ * outside the input's chunks is E_INVAL.  Partial containers are combined
+ * with dlmc_merge; dlmc_decode accepts only complete containers.  The bound
+ * call gives the worst-case size of such a partial container. */
+dlmc_status dlmc_encode_range(dlmc_model* model, const dlmc_codec_params* codec,
+                              const int32_t* tokens, uint64_t n, uint64_t first_chunk,
+                              uint64_t n_chunks, uint8_t* out, uint64_t cap, uint64_t* out_len);
+dlmc_status dlmc_encode_range_bound(const dlmc_model* model, const dlmc_codec_params* codec,
+                                    uint64_t n_tokens, uint64_t first_chunk, uint64_t n_chunks,
+                                    uint64_t* bytes);
+/* Combine n_parts host containers (parts[i] of lens[i] bytes, in any order)
+ * of the same input, model, build and codec parameters whose chunk ranges
+ * tile all of the input's chunks into one complete container in out[0..cap),
+ * byte-identical to dlmc_encode of the whole input.  No GPU is used.
+ * E_FORMAT if the parts disagree in any header field, overlap, or leave a
+ * chunk out; E_BUFFER as for dlmc_encode. */
+dlmc_status dlmc_merge(const uint8_t* const* parts, const uint64_t* lens, int32_t n_parts,
+                       uint8_t* out, uint64_t cap, uint64_t* out_len);
+/* Number of tokens a container holds (reads the header only; E_FORMAT, also
+ * for a container made by a build with another numerics identity). */
 dlmc_status dlmc_decode_size(const uint8_t* in, uint64_t len, uint64_t* n_tokens);
+/* The 64-bit numerics identity of this build: a hash of the library's source
+ * code and compile flags.  Every container records the identity of the build
+ * that made it, and a build with another identity refuses to decode it
+ * (E_FORMAT): the decoder must replay the encoder's decisions exactly (the
+ * remark closing Symbol Commitment Schedules), and kernels that round
+ * differently could take other decisions. */
+dlmc_status dlmc_numerics_id(uint64_t* id);
 /* Decompress host container in[0..len) into host tokens[0..cap).  The codec
  * parameters come from the header; the batch used is `batch` when > 0, else
  * the header's.  E_FORMAT if the container was made by a model with another
@@ -191,15 +241,25 @@ dlmc_status dlmc_encoder_step(dlmc_session* s, int32_t* done, uint64_t* coded);
 dlmc_status dlmc_encoder_finish(dlmc_session* s, uint8_t* out, uint64_t cap, uint64_t* out_len);
 void dlmc_session_destroy(dlmc_session* s);
 
-/* Per (chunk, pass) trace of encode and decode: the committed positions
- * (ascending), their entropies in bits, and an FNV-1a 64 hash of the
- * committed rows' integer CDFs.  dir = 0 encode, 1 decode.  NULL disables. */
+/* Per (chunk, pass) trace of encode and decode (arrays valid during the
+ * call only): the n_sel committed positions pos[] (ascending), their
+ * entropies in bits, the coded pairs coded[2 j], coded[2 j + 1] of position
+ * pos[j] -- the interval (start, freq) of its symbol in the 2^cdf_bits total
+ * for the range and rANS coders, (rank, symbol) for symbol ranking -- and an
+ * FNV-1a 64 hash of the committed rows' integer CDFs (of the coded symbols
+ * for symbol ranking).  dir = 0 encode, 1 decode.  Encode and decode of the
+ * same container report identical traces.  NULL disables. */
 typedef void (*dlmc_trace_fn)(void* user, int32_t dir, uint64_t chunk, int32_t pass,
                               int32_t n_sel, const int32_t* pos, const float* entropy_bits,
-                              uint64_t cdf_hash);
+                              const uint32_t* coded, uint64_t cdf_hash);
 dlmc_status dlmc_set_trace(dlmc_model* model, dlmc_trace_fn fn, void* user);
 
 /* ---- stage hooks (device pointers; tests and benchmarks) ---------------- */
+
+/* Test hook for the error path of non-finite model output: while `on` is
+ * nonzero, every forward pass of the model writes a NaN into the first logit
+ * of its first head row, so that encoding fails with E_NUMERIC. */
+dlmc_status dlmc_test_inject_nonfinite(dlmc_model* model, int32_t on);
 
 /* One forward pass (Definition 3) over device state[B*T] (int32, MASK =
  * vocab).  Writes the fp32 logits at the masked positions, in ascending

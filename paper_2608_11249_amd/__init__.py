@@ -72,7 +72,8 @@ CONTEXT = {"contiguous": 0, "random": 1, "attention": 2}
 
 TRACE_FN = ctypes.CFUNCTYPE(None, ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint64,
                             ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32),
-                            ctypes.POINTER(ctypes.c_float), ctypes.c_uint64)
+                            ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_uint32),
+                            ctypes.c_uint64)
 
 _lib = None
 P = ctypes.POINTER
@@ -103,6 +104,11 @@ _SIGS = {
     "dlmc_context_scores": (i32, [vp, vp, i32, vp]),
     "dlmc_select_rank_rows": (i32, [vp, vp, i32, vp, vp]),
     "dlmc_rans_decode": (i32, [vp, u64, vp, u64, i32, i32, vp]),
+    "dlmc_encode_range": (i32, [vp, P(CodecParams), vp, u64, u64, u64, vp, u64, P(u64)]),
+    "dlmc_encode_range_bound": (i32, [vp, P(CodecParams), u64, u64, u64, P(u64)]),
+    "dlmc_merge": (i32, [P(vp), P(u64), i32, vp, u64, P(u64)]),
+    "dlmc_numerics_id": (i32, [P(u64)]),
+    "dlmc_test_inject_nonfinite": (i32, [vp, i32]),
     "dlmc_status_string": (ctypes.c_char_p, [i32]),
     "dlmc_last_error": (ctypes.c_char_p, []),
 }
@@ -245,6 +251,25 @@ class Model:
                                  bound, ctypes.byref(n)))
         return out[: n.value].tobytes()
 
+    def encode_range(self, tokens, codec, first_chunk: int, n_chunks: int, batch=None,
+                     crc=False) -> bytes:
+        """A partial container of chunks [first_chunk, first_chunk + n_chunks)."""
+        tok = np.ascontiguousarray(tokens, dtype=np.int32)
+        cp = codec_params(codec, batch, crc)
+        bound = u64(0)
+        _check(lib().dlmc_encode_range_bound(self.handle, ctypes.byref(cp), len(tok), first_chunk,
+                                             n_chunks, ctypes.byref(bound)))
+        out = np.empty(max(bound.value, 1), dtype=np.uint8)
+        n = u64(0)
+        _check(lib().dlmc_encode_range(self.handle, ctypes.byref(cp), _ptr(tok), len(tok),
+                                       first_chunk, n_chunks, _ptr(out), bound.value,
+                                       ctypes.byref(n)))
+        return out[: n.value].tobytes()
+
+    def inject_nonfinite(self, on: bool):
+        """Test hook: every forward writes a NaN into its first logit while on."""
+        _check(lib().dlmc_test_inject_nonfinite(self.handle, 1 if on else 0))
+
     def decode(self, data: bytes, batch: int = 0) -> np.ndarray:
         buf = np.frombuffer(data, dtype=np.uint8).copy()
         n = decode_size(data)
@@ -257,16 +282,23 @@ class Model:
     def encoder(self, codec, tokens, batch=None, crc=False) -> Encoder:
         return Encoder(self, codec, tokens, batch, crc)
 
-    def set_trace(self, fn: Optional[Callable]):
-        """fn(dir, chunk, pass, positions: list, entropies: list, cdf_hash) or None."""
+    def set_trace(self, fn: Optional[Callable], coded: bool = False):
+        """fn(dir, chunk, pass, positions: list, entropies: list, cdf_hash) or
+        None; with coded=True fn(dir, chunk, pass, positions, entropies,
+        coded_pairs: list of (start, freq) / (rank, symbol), cdf_hash)."""
         if fn is None:
             self._trace_cb = None
             _check(lib().dlmc_set_trace(self.handle, TRACE_FN(), None))
             return
 
-        def cb(_user, d, chunk, pas, n, pos, ent, hsh):
-            fn(int(d), int(chunk), int(pas), [pos[i] for i in range(n)],
-               [ent[i] for i in range(n)], int(hsh))
+        def cb(_user, d, chunk, pas, n, pos, ent, iv, hsh):
+            p = [pos[i] for i in range(n)]
+            e = [ent[i] for i in range(n)]
+            if coded:
+                fn(int(d), int(chunk), int(pas), p, e,
+                   [(int(iv[2 * i]), int(iv[2 * i + 1])) for i in range(n)], int(hsh))
+            else:
+                fn(int(d), int(chunk), int(pas), p, e, int(hsh))
 
         self._trace_cb = TRACE_FN(cb)
         _check(lib().dlmc_set_trace(self.handle, self._trace_cb, None))
@@ -387,6 +419,28 @@ def decode_size(data: bytes) -> int:
     n = u64(0)
     _check(lib().dlmc_decode_size(_ptr(buf) if len(buf) else None, len(buf), ctypes.byref(n)))
     return n.value
+
+
+def merge(parts: Sequence[bytes]) -> bytes:
+    """One complete container from partial containers of the same input."""
+    bufs = [np.frombuffer(p, dtype=np.uint8).copy() for p in parts]
+    ptrs = (vp * len(bufs))(*[b.ctypes.data if len(b) else None for b in bufs])
+    lens = (u64 * len(bufs))(*[len(b) for b in bufs])
+    n = u64(0)
+    L = lib()
+    st = L.dlmc_merge(ptrs, lens, len(bufs), None, 0, ctypes.byref(n))
+    if st != -6:
+        _check(st)
+    out = np.empty(max(n.value, 1), dtype=np.uint8)
+    _check(L.dlmc_merge(ptrs, lens, len(bufs), _ptr(out), n.value, ctypes.byref(n)))
+    return out[: n.value].tobytes()
+
+
+def numerics_id() -> int:
+    """This build's numerics identity (recorded in every container)."""
+    out = u64(0)
+    _check(lib().dlmc_numerics_id(ctypes.byref(out)))
+    return out.value
 
 
 def rc_encode(start, freq, cdf_bits: int, coder_bits: int) -> bytes:

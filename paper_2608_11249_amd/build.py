@@ -31,10 +31,36 @@ LIBS = ["-lz", "-ldl"]
 EXTRA = {"attention.hip": ["-fno-honor-nans"]}
 
 
+def _code(path: str) -> str:
+    """A source file's code: // comments, trailing blanks and empty lines removed."""
+    lines = []
+    for line in open(path, encoding="utf-8"):
+        line = line.split("//", 1)[0].rstrip()
+        if line:
+            lines.append(line)
+    return "\n".join(lines)
+
+
+def numerics_id() -> int:
+    """64-bit identity of the library's arithmetic: a SHA-256 of the code of every
+    source and header (comments stripped) and of the compile flags.  Containers
+    record it; a build with another identity refuses to decode them, since
+    kernels that round differently would replay other decisions."""
+    import hashlib
+    h = hashlib.sha256()
+    files = sorted(f for f in os.listdir(CSRC) if f.endswith((".hip", ".cpp", ".h")))
+    for f in files:
+        h.update(f.encode() + b"\0" + _code(os.path.join(CSRC, f)).encode() + b"\0")
+    h.update(_code(os.path.join(os.path.dirname(HERE), "include", "dlmc.h")).encode())
+    h.update(repr((COMMON, sorted(EXTRA.items()))).encode())
+    return int.from_bytes(h.digest()[:8], "little")
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, src.rsplit(".", 1)[0] + ".o")
     lang = ["-x", "hip"] if src.endswith(".hip") else []
-    cmd = [HIPCC, *COMMON, *EXTRA.get(src, []), *lang, "-c", os.path.join(CSRC, src), "-o", obj]
+    ident = [f"-DDLMC_NUMERICS_ID=0x{numerics_id():016x}ull"] if src == "session.cpp" else []
+    cmd = [HIPCC, *COMMON, *EXTRA.get(src, []), *ident, *lang, "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"compile of {src} failed:\n{r.stderr}")

@@ -10,11 +10,8 @@ using namespace dlmc;
 
 namespace dlmc {
 dlmc_session* make_encoder(dlmc_model* m, const dlmc_codec_params& cp, const int32_t* tokens,
-                           uint64_t n);
+                           uint64_t n, uint64_t first_chunk, uint64_t n_range);
 dlmc_session* make_decoder(dlmc_model* m, const uint8_t* in, uint64_t len, int32_t batch);
-void parse_header(const uint8_t* in, uint64_t len, dlmc_codec_params* cp, uint64_t* n,
-                  uint64_t* n_chunks, uint64_t* hash, uint64_t* seed, uint32_t* hdr);
-uint64_t encode_bound(const dlmc_codec_params& cp, uint64_t n);
 }  // namespace dlmc
 
 namespace {
@@ -42,6 +39,27 @@ void use(dlmc_model* m) {
   DLMC_CHECK(m, DLMC_E_INVAL, "model is NULL");
   DLMC_HIP(hipSetDevice(m->device));
 }
+
+// Device buffers of one call, freed when it returns or throws.
+struct DevBufs {
+  std::vector<void*> held;
+  template <typename T>
+  T* alloc(size_t bytes) {
+    void* q = nullptr;
+    if (hipMalloc(&q, std::max<size_t>(bytes, 16)) != hipSuccess || !q) {
+      (void)hipGetLastError();
+      throw Error(DLMC_E_NOMEM, "hipMalloc of " + std::to_string(bytes) + " bytes failed");
+    }
+    held.push_back(q);
+    return (T*)q;
+  }
+  DevBufs() = default;
+  DevBufs(const DevBufs&) = delete;
+  DevBufs& operator=(const DevBufs&) = delete;
+  ~DevBufs() {
+    for (void* q : held) (void)hipFree(q);  // hipFree waits for the device
+  }
+};
 
 dlmc_status write_out(const std::vector<uint8_t>& bytes, uint8_t* out, uint64_t cap,
                       uint64_t* out_len) {
@@ -89,7 +107,17 @@ dlmc_status dlmc_encode_bound(const dlmc_model* m, const dlmc_codec_params* code
   return guard([&] {
     DLMC_CHECK(m && codec && bytes, DLMC_E_INVAL, "NULL argument");
     validate_codec(m, *codec);
-    *bytes = encode_bound(*codec, n_tokens);
+    *bytes = encode_bound(*codec, n_tokens, 0, UINT64_MAX);
+  });
+}
+
+dlmc_status dlmc_encode_range_bound(const dlmc_model* m, const dlmc_codec_params* codec,
+                                    uint64_t n_tokens, uint64_t first_chunk, uint64_t n_chunks,
+                                    uint64_t* bytes) {
+  return guard([&] {
+    DLMC_CHECK(m && codec && bytes, DLMC_E_INVAL, "NULL argument");
+    validate_codec(m, *codec);
+    *bytes = encode_bound(*codec, n_tokens, first_chunk, n_chunks);
   });
 }
 
@@ -98,7 +126,7 @@ dlmc_status dlmc_encoder_begin(dlmc_model* m, const dlmc_codec_params* codec,
   return guard([&] {
     use(m);
     DLMC_CHECK(codec && out, DLMC_E_INVAL, "NULL argument");
-    *out = make_encoder(m, *codec, tokens, n);
+    *out = make_encoder(m, *codec, tokens, n, 0, UINT64_MAX);
   });
 }
 
@@ -134,13 +162,42 @@ dlmc_status dlmc_encode(dlmc_model* m, const dlmc_codec_params* codec, const int
   return st;
 }
 
+dlmc_status dlmc_encode_range(dlmc_model* m, const dlmc_codec_params* codec, const int32_t* tokens,
+                              uint64_t n, uint64_t first_chunk, uint64_t n_chunks, uint8_t* out,
+                              uint64_t cap, uint64_t* out_len) {
+  dlmc_session* s = nullptr;
+  dlmc_status st = guard([&] {
+    use(m);
+    DLMC_CHECK(codec, DLMC_E_INVAL, "NULL argument");
+    s = make_encoder(m, *codec, tokens, n, first_chunk, n_chunks);
+  });
+  if (st != DLMC_OK) return st;
+  st = dlmc_encoder_finish(s, out, cap, out_len);
+  delete s;
+  return st;
+}
+
+dlmc_status dlmc_merge(const uint8_t* const* parts, const uint64_t* lens, int32_t n_parts,
+                       uint8_t* out, uint64_t cap, uint64_t* out_len) {
+  std::vector<uint8_t> bytes;
+  dlmc_status st = guard([&] { bytes = merge_containers(parts, lens, n_parts); });
+  if (st != DLMC_OK) return st;
+  return write_out(bytes, out, cap, out_len);
+}
+
+dlmc_status dlmc_numerics_id(uint64_t* id) {
+  return guard([&] {
+    DLMC_CHECK(id, DLMC_E_INVAL, "NULL argument");
+    *id = numerics_id();
+  });
+}
+
 dlmc_status dlmc_decode_size(const uint8_t* in, uint64_t len, uint64_t* n_tokens) {
   return guard([&] {
     DLMC_CHECK(n_tokens, DLMC_E_INVAL, "NULL argument");
-    dlmc_codec_params cp{};
-    uint64_t nc, hash, seed;
-    uint32_t hdr;
-    parse_header(in, len, &cp, n_tokens, &nc, &hash, &seed, &hdr);
+    ContainerInfo ci;
+    parse_header(in, len, &ci);
+    *n_tokens = ci.n;
   });
 }
 
@@ -169,6 +226,13 @@ dlmc_status dlmc_set_trace(dlmc_model* m, dlmc_trace_fn fn, void* user) {
   });
 }
 
+dlmc_status dlmc_test_inject_nonfinite(dlmc_model* m, int32_t on) {
+  return guard([&] {
+    DLMC_CHECK(m, DLMC_E_INVAL, "model is NULL");
+    m->inject_nan = on != 0;
+  });
+}
+
 dlmc_status dlmc_forward_logits(dlmc_model* m, const int32_t* state, int32_t B, int32_t T,
                                 float* logits, int32_t* rows, int32_t* n_rows) {
   return guard([&] {
@@ -186,24 +250,24 @@ dlmc_status dlmc_entropy_cdf(dlmc_model* m, const float* logits, int32_t n_rows,
     DLMC_CHECK(logits && entropy_bits && row_max && n_rows >= 0, DLMC_E_INVAL, "bad argument");
     const int V = m->cfg.vocab;
     hipStream_t s = m->stream;
+    if (cdf) {
+      DLMC_CHECK(cdf_bits >= 2 && cdf_bits <= 31 && (1ll << cdf_bits) > V, DLMC_E_INVAL,
+                 "cdf_bits must be in 2..31 with 2^cdf_bits > vocab");
+      DLMC_CHECK(n_rows <= 65535, DLMC_E_INVAL, "at most 65535 CDF rows per call");
+    }
     entropy_rows(s, logits, n_rows, nullptr, V, entropy_bits, row_max);
     if (cdf && n_rows > 0) {
       // every row committed: one "chunk" per row, n_sel = 1
-      DLMC_CHECK(n_rows <= 65535, DLMC_E_INVAL, "at most 65535 CDF rows per call");
-      int32_t *sel_row = nullptr, *n_sel = nullptr;
-      void* ws = nullptr;
-      DLMC_HIP(hipMalloc((void**)&sel_row, (size_t)n_rows * 4));
-      DLMC_HIP(hipMalloc((void**)&n_sel, (size_t)n_rows * 4));
-      DLMC_HIP(hipMalloc(&ws, cdf_workspace_bytes(n_rows, V)));
+      DevBufs bufs;
+      int32_t* sel_row = bufs.alloc<int32_t>((size_t)n_rows * 4);
+      int32_t* n_sel = bufs.alloc<int32_t>((size_t)n_rows * 4);
+      void* ws = bufs.alloc<void>(cdf_workspace_bytes(n_rows, V));
       std::vector<int32_t> idx(n_rows), one(n_rows, 1);
       for (int i = 0; i < n_rows; ++i) idx[i] = i;
       DLMC_HIP(hipMemcpyAsync(sel_row, idx.data(), idx.size() * 4, hipMemcpyHostToDevice, s));
       DLMC_HIP(hipMemcpyAsync(n_sel, one.data(), one.size() * 4, hipMemcpyHostToDevice, s));
       cdf_rows(s, logits, row_max, sel_row, n_sel, n_rows, 1, V, cdf_bits, cdf, g, ws);
       DLMC_HIP(hipStreamSynchronize(s));
-      (void)hipFree(sel_row);
-      (void)hipFree(n_sel);
-      (void)hipFree(ws);
     }
     DLMC_HIP(hipStreamSynchronize(s));
   });
@@ -317,16 +381,17 @@ dlmc_status dlmc_profile_read(dlmc_model* m, int32_t stage, double* ms_total, ui
 namespace {
 // one "chunk" of length 1 per row: slot i commits position 0 of row i
 struct RowSlots {
+  DevBufs bufs;
   int32_t *sel_row = nullptr, *sel_pos = nullptr, *n_sel = nullptr, *state = nullptr;
   int64_t* base = nullptr;
   uint32_t* pairs = nullptr;
   explicit RowSlots(int n, hipStream_t s) {
-    DLMC_HIP(hipMalloc((void**)&sel_row, (size_t)n * 4));
-    DLMC_HIP(hipMalloc((void**)&sel_pos, (size_t)n * 4));
-    DLMC_HIP(hipMalloc((void**)&n_sel, (size_t)n * 4));
-    DLMC_HIP(hipMalloc((void**)&state, (size_t)n * 4));
-    DLMC_HIP(hipMalloc((void**)&base, (size_t)n * 8));
-    DLMC_HIP(hipMalloc((void**)&pairs, (size_t)n * 8));
+    sel_row = bufs.alloc<int32_t>((size_t)n * 4);
+    sel_pos = bufs.alloc<int32_t>((size_t)n * 4);
+    n_sel = bufs.alloc<int32_t>((size_t)n * 4);
+    state = bufs.alloc<int32_t>((size_t)n * 4);
+    base = bufs.alloc<int64_t>((size_t)n * 8);
+    pairs = bufs.alloc<uint32_t>((size_t)n * 8);
     std::vector<int32_t> idx(n), zero(n, 0), one(n, 1);
     std::vector<int64_t> b(n);
     for (int i = 0; i < n; ++i) idx[i] = i, b[i] = i;
@@ -335,14 +400,6 @@ struct RowSlots {
     DLMC_HIP(hipMemcpyAsync(n_sel, one.data(), (size_t)n * 4, hipMemcpyHostToDevice, s));
     DLMC_HIP(hipMemcpyAsync(base, b.data(), (size_t)n * 8, hipMemcpyHostToDevice, s));
     DLMC_HIP(hipStreamSynchronize(s));
-  }
-  ~RowSlots() {
-    (void)hipFree(sel_row);
-    (void)hipFree(sel_pos);
-    (void)hipFree(n_sel);
-    (void)hipFree(state);
-    (void)hipFree(base);
-    (void)hipFree(pairs);
   }
 };
 }  // namespace

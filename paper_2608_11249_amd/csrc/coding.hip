@@ -287,10 +287,13 @@ __global__ void __launch_bounds__(256) cdf_pass_a(CdfArgs c) {
   }
 }
 
+// G of a row.  A finite row maximum gives G >= 2^24; a row of non-finite
+// logits (reported as E_NUMERIC before its CDF is used) can give 0, which is
+// raised to 1 so that the divisions below stay defined.
 __device__ __forceinline__ uint64_t row_G(const CdfArgs& c, int slot) {
   uint64_t G = 0;
   for (int s = 0; s < c.S; ++s) G += c.segG[(size_t)slot * c.S + s];
-  return G;
+  return G > 0 ? G : 1;
 }
 
 __global__ void __launch_bounds__(256) cdf_pass_b(CdfArgs c) {
@@ -376,6 +379,11 @@ __global__ void __launch_bounds__(256) cdf_pass_c(CdfArgs c) {
   }
 }
 
+// a quiet NaN in the first logit of the first row, if any row exists
+__global__ void poison_kernel(float* __restrict__ logits, const int32_t* __restrict__ n_dev) {
+  if (threadIdx.x == 0 && n_dev[0] > 0) logits[0] = __builtin_nanf("");
+}
+
 // ---------------------------------------------------------------- reveal
 __global__ void gather_reveal_kernel(const uint32_t* __restrict__ cdf, const int32_t* __restrict__ sel_pos,
                                      const int32_t* __restrict__ n_sel, const int32_t* __restrict__ tokens,
@@ -457,6 +465,11 @@ void cdf_rows(hipStream_t st, const float* logits, const float* mx, const int32_
   cdf_pass_a<<<grid, 256, 0, st>>>(c);
   cdf_pass_b<<<grid, 256, 0, st>>>(c);
   cdf_pass_c<<<grid, 256, 0, st>>>(c);
+  DLMC_HIP(hipGetLastError());
+}
+
+void poison_first_logit(hipStream_t st, float* logits, const int32_t* n_dev) {
+  poison_kernel<<<1, 64, 0, st>>>(logits, n_dev);
   DLMC_HIP(hipGetLastError());
 }
 

@@ -87,6 +87,8 @@ inline size_t cdf_workspace_bytes(size_t slots, int V) {
 void cdf_rows(hipStream_t st, const float* logits, const float* mx, const int32_t* sel_row,
               const int32_t* n_sel, int B, int m_max, int V, int P, uint32_t* cdf,
               uint32_t* g_out, void* seg_ws);
+// test hook: a NaN into logits[0] when n_dev[0] > 0
+void poison_first_logit(hipStream_t st, float* logits, const int32_t* n_dev);
 // encode: (start, freq) of the true symbol of every committed position and reveal it
 void gather_reveal(hipStream_t st, const uint32_t* cdf, const int32_t* sel_pos,
                    const int32_t* n_sel, const int32_t* tokens, const int64_t* slot_base,

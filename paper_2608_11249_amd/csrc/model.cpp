@@ -186,47 +186,22 @@ void create_model(dlmc_model* m, const dlmc_model_config& cfg, uint64_t seed, in
   const int nF = glu ? 2 * F : F;
   hipStream_t st = m->stream;
 
+  // every buffer is allocated before any kernel runs, so a model that does
+  // not fit fails with E_NOMEM and nothing launched
   // ---- weights
   m->embed = m->dalloc((size_t)(V + 1) * d * m->esz);
-  init_weights(st, m->embed, dt, seed, 1, V + 1, d, cfg.embed_exp, MAP_IDENTITY, 0, dh);
   m->head = m->dalloc((size_t)V * d * m->esz);
-  init_weights(st, m->head, dt, seed, 2, V, d, cfg.head_exp, MAP_IDENTITY, 0, dh);
-  const RowMap qk_map = m->bf16 ? MAP_QK_PAIRS : MAP_IDENTITY;
   for (int l = 0; l < L; ++l) {
     dlmc_model::Layer w{};
-    const int base = 16 + 16 * l;
     w.wqkv = m->dalloc((size_t)3 * d * d * m->esz);
-    init_weights(st, w.wqkv, dt, seed, base + 0, d, d, cfg.attn_exp, qk_map, 0, dh);
-    init_weights(st, w.wqkv, dt, seed, base + 1, d, d, cfg.attn_exp, qk_map, d, dh);
-    init_weights(st, w.wqkv, dt, seed, base + 2, d, d, cfg.attn_exp, MAP_IDENTITY, 2 * d, dh);
     w.wo = m->dalloc((size_t)d * d * m->esz);
-    init_weights(st, w.wo, dt, seed, base + 3, d, d, cfg.attn_exp, MAP_IDENTITY, 0, dh);
     w.win = m->dalloc((size_t)nF * d * m->esz);
-    if (glu && m->bf16) {
-      init_weights(st, w.win, dt, seed, base + 4, F, d, cfg.ffn_in_exp, MAP_GLU_PAIRS, 0, dh);
-      init_weights(st, w.win, dt, seed, base + 5, F, d, cfg.ffn_in_exp, MAP_GLU_PAIRS, 32, dh);
-    } else {
-      init_weights(st, w.win, dt, seed, base + 4, F, d, cfg.ffn_in_exp, MAP_IDENTITY, 0, dh);
-      if (glu) init_weights(st, w.win, dt, seed, base + 5, F, d, cfg.ffn_in_exp, MAP_IDENTITY, F, dh);
-    }
     w.wout = m->dalloc((size_t)d * F * m->esz);
-    init_weights(st, w.wout, dt, seed, base + 6, d, F, cfg.ffn_out_exp, MAP_IDENTITY, 0, dh);
     m->layers.push_back(w);
   }
-
-  // ---- rotary table: angle = t * theta^(-2i/dh), computed in fp64
   const int half = dh / 2, T = cfg.max_chunk;
-  std::vector<float> cs((size_t)T * half), sn((size_t)T * half);
-  for (int t = 0; t < T; ++t)
-    for (int i = 0; i < half; ++i) {
-      const double ang = (double)t * std::pow((double)cfg.rope_theta, -2.0 * i / dh);
-      cs[(size_t)t * half + i] = (float)std::cos(ang);
-      sn[(size_t)t * half + i] = (float)std::sin(ang);
-    }
-  m->rope_cos = (float*)m->dalloc(cs.size() * 4);
-  m->rope_sin = (float*)m->dalloc(sn.size() * 4);
-  DLMC_HIP(hipMemcpyAsync(m->rope_cos, cs.data(), cs.size() * 4, hipMemcpyHostToDevice, st));
-  DLMC_HIP(hipMemcpyAsync(m->rope_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice, st));
+  m->rope_cos = (float*)m->dalloc((size_t)T * half * 4);
+  m->rope_sin = (float*)m->dalloc((size_t)T * half * 4);
 
   // ---- workspace
   const size_t R = (size_t)cfg.max_batch * cfg.max_chunk;
@@ -235,10 +210,9 @@ void create_model(dlmc_model* m, const dlmc_model_config& cfg, uint64_t seed, in
   const size_t qkv_elems = (size_t)cfg.max_batch * H * m->Tp_max * dh;
   m->x = (float*)m->dalloc(R * d * 4);
   m->h = m->dalloc(R * d * m->esz);
-  // Q, K, V^T padding rows are read (with zero weight) by attention: keep them finite
-  m->q = m->dalloc(qkv_elems * m->esz, true);
-  m->k = m->dalloc(qkv_elems * m->esz, true);
-  m->vt = m->dalloc(qkv_elems * m->esz, true);
+  m->q = m->dalloc(qkv_elems * m->esz);
+  m->k = m->dalloc(qkv_elems * m->esz);
+  m->vt = m->dalloc(qkv_elems * m->esz);
   m->attn = m->dalloc(R * d * m->esz);
   m->ffn = m->dalloc(R * F * m->esz);
   if (!m->bf16) m->tmp = (float*)m->dalloc(R * std::max(3 * d, nF) * 4);
@@ -247,11 +221,50 @@ void create_model(dlmc_model* m, const dlmc_model_config& cfg, uint64_t seed, in
   m->H = (float*)m->dalloc(R * 4);
   m->mx = (float*)m->dalloc(R * 4);
   m->rows = (int32_t*)m->dalloc(R * 4);
-  m->n_rows = (int32_t*)m->dalloc(4, true);
+  m->n_rows = (int32_t*)m->dalloc(4);
   m->chunk_off = (int32_t*)m->dalloc((size_t)cfg.max_batch * 4);
   m->chunk_cnt = (int32_t*)m->dalloc((size_t)cfg.max_batch * 4);
   m->state = (int32_t*)m->dalloc(R * 4);
-  m->err = (int32_t*)m->dalloc(4, true);
+  m->err = (int32_t*)m->dalloc(4);
+
+  // Q, K, V^T padding rows are read (with zero weight) by attention: keep them finite
+  DLMC_HIP(hipMemsetAsync(m->q, 0, qkv_elems * m->esz, st));
+  DLMC_HIP(hipMemsetAsync(m->k, 0, qkv_elems * m->esz, st));
+  DLMC_HIP(hipMemsetAsync(m->vt, 0, qkv_elems * m->esz, st));
+  DLMC_HIP(hipMemsetAsync(m->n_rows, 0, 4, st));
+  DLMC_HIP(hipMemsetAsync(m->err, 0, 4, st));
+
+  // ---- weight generation
+  init_weights(st, m->embed, dt, seed, 1, V + 1, d, cfg.embed_exp, MAP_IDENTITY, 0, dh);
+  init_weights(st, m->head, dt, seed, 2, V, d, cfg.head_exp, MAP_IDENTITY, 0, dh);
+  const RowMap qk_map = m->bf16 ? MAP_QK_PAIRS : MAP_IDENTITY;
+  for (int l = 0; l < L; ++l) {
+    const dlmc_model::Layer& w = m->layers[l];
+    const int base = 16 + 16 * l;
+    init_weights(st, w.wqkv, dt, seed, base + 0, d, d, cfg.attn_exp, qk_map, 0, dh);
+    init_weights(st, w.wqkv, dt, seed, base + 1, d, d, cfg.attn_exp, qk_map, d, dh);
+    init_weights(st, w.wqkv, dt, seed, base + 2, d, d, cfg.attn_exp, MAP_IDENTITY, 2 * d, dh);
+    init_weights(st, w.wo, dt, seed, base + 3, d, d, cfg.attn_exp, MAP_IDENTITY, 0, dh);
+    if (glu && m->bf16) {
+      init_weights(st, w.win, dt, seed, base + 4, F, d, cfg.ffn_in_exp, MAP_GLU_PAIRS, 0, dh);
+      init_weights(st, w.win, dt, seed, base + 5, F, d, cfg.ffn_in_exp, MAP_GLU_PAIRS, 32, dh);
+    } else {
+      init_weights(st, w.win, dt, seed, base + 4, F, d, cfg.ffn_in_exp, MAP_IDENTITY, 0, dh);
+      if (glu) init_weights(st, w.win, dt, seed, base + 5, F, d, cfg.ffn_in_exp, MAP_IDENTITY, F, dh);
+    }
+    init_weights(st, w.wout, dt, seed, base + 6, d, F, cfg.ffn_out_exp, MAP_IDENTITY, 0, dh);
+  }
+
+  // ---- rotary table: angle = t * theta^(-2i/dh), computed in fp64
+  std::vector<float> cs((size_t)T * half), sn((size_t)T * half);
+  for (int t = 0; t < T; ++t)
+    for (int i = 0; i < half; ++i) {
+      const double ang = (double)t * std::pow((double)cfg.rope_theta, -2.0 * i / dh);
+      cs[(size_t)t * half + i] = (float)std::cos(ang);
+      sn[(size_t)t * half + i] = (float)std::sin(ang);
+    }
+  DLMC_HIP(hipMemcpyAsync(m->rope_cos, cs.data(), cs.size() * 4, hipMemcpyHostToDevice, st));
+  DLMC_HIP(hipMemcpyAsync(m->rope_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice, st));
   DLMC_HIP(hipStreamSynchronize(st));
 }
 
@@ -420,6 +433,7 @@ void dlmc_model::forward(const int32_t* st_dev, int B, int T, float* logits_out,
               rows_hint >= 0 ? (int)rows_hint : -1);
   else
     gemm_f32(s, (const float*)hm, (const float*)this->head, M, V, d, nr, EPI_STORE_F32, o);
+  if (inject_nan) poison_first_logit(s, lg, nr);
 }
 
 void dlmc_model::context_scores(const int32_t* tokens, int T, std::vector<float>& score) {

@@ -52,6 +52,7 @@ struct dlmc_model {
   int32_t* tokens_dev = nullptr;
   size_t tokens_cap = 0;
 
+  bool inject_nan = false;  // test hook: a NaN into the first logit of every forward
   dlmc_trace_fn trace = nullptr;
   void* trace_user = nullptr;
 
@@ -126,6 +127,19 @@ std::vector<uint8_t> compress_block(int kind, int level, const std::vector<uint8
 std::vector<uint8_t> decompress_block(int kind, const uint8_t* in, size_t len, size_t expect);
 
 uint64_t fnv1a64(const void* data, size_t n, uint64_t h = 0xCBF29CE484222325ull);
+
+// Parsed fixed header of a container (include/dlmc.h describes the layout).
+struct ContainerInfo {
+  dlmc_codec_params cp{};
+  uint64_t n = 0, n_chunks = 0, hash = 0, seed = 0;
+  uint64_t first = 0, count = 0;  // held chunk range
+  uint64_t total = 0;             // bytes of the (uncompressed) payload section
+  uint32_t hdr = 0;               // header bytes before the payload section
+};
+void parse_header(const uint8_t* in, uint64_t len, ContainerInfo* ci);
+std::vector<uint8_t> merge_containers(const uint8_t* const* parts, const uint64_t* lens, int n_parts);
+uint64_t encode_bound(const dlmc_codec_params& cp, uint64_t n, uint64_t first, uint64_t count);
+uint64_t numerics_id();
 uint32_t crc32(const void* data, size_t n);
 void create_model(dlmc_model* m, const dlmc_model_config& cfg, uint64_t seed, int device);
 void validate_codec(const dlmc_model* m, const dlmc_codec_params& cp);
@@ -141,6 +155,7 @@ struct dlmc_session {
   std::vector<std::vector<uint8_t>> payload;  // per chunk (encode output / decode input)
   std::vector<uint32_t> crc;                  // per chunk (decode: expected)
   uint64_t n_chunks = 0, n_full = 0;
+  uint64_t first_chunk = 0, end_chunk = 0;  // the chunk range [first, end) coded here
   int last_len = 0;
 
   // pass-loop state
@@ -157,6 +172,7 @@ struct dlmc_session {
   std::vector<std::vector<uint8_t>> rk_out;
   std::vector<const uint8_t*> rk_data;
   std::vector<size_t> rk_len, rk_pos;
+  std::vector<int32_t> rk_rank;  // decode: the ranks of the current pass (trace)
   // initial context and left-to-right block schedules
   std::vector<std::vector<int32_t>> slot_ctx_pos, slot_ctx_sym;  // per slot
   std::vector<std::vector<int32_t>> slot_order;  // masked positions, ascending

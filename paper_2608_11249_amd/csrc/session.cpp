@@ -19,8 +19,17 @@ using namespace dlmc;
 namespace {
 
 constexpr uint32_t MAGIC = 0x434D4C44u;  // "DLMC" little endian
-constexpr uint32_t VERSION = 2;
-constexpr size_t FIXED_HEADER = 120;
+constexpr uint32_t VERSION = 3;
+constexpr size_t FIXED_HEADER = 144;
+
+// Identity of this build's arithmetic: a hash of the library's source code and
+// compile flags, set by the build.  The same input coded by two builds whose
+// kernels round differently gives different decisions, so a container only
+// decodes under the build identity it was made with.
+#ifndef DLMC_NUMERICS_ID
+#error "DLMC_NUMERICS_ID must be defined by the build (hash of the sources and flags)"
+#endif
+constexpr uint64_t NUMERICS_ID = DLMC_NUMERICS_ID;
 
 template <typename T>
 void put(std::vector<uint8_t>& v, size_t off, T x) {
@@ -225,18 +234,23 @@ void dlmc_session::assign(int b, uint64_t chunk) {
 
 void dlmc_session::begin_phase() {
   if (phase == 0) {
-    B = (int)std::min<uint64_t>((uint64_t)cp.batch, std::max<uint64_t>(n_full, 1));
+    // full-length chunks of the range [first_chunk, end_chunk)
+    const uint64_t hi = std::min(end_chunk, n_full);
+    const uint64_t cnt = hi > first_chunk ? hi - first_chunk : 0;
+    B = (int)std::min<uint64_t>((uint64_t)cp.batch, std::max<uint64_t>(cnt, 1));
     T = cp.chunk_len;
-    if (n_full == 0) {
+    if (cnt == 0) {
       phase = 1;
       begin_phase();
       return;
     }
   } else if (phase == 1) {
-    if (n_chunks == n_full) {
+    // the final partial chunk, when it exists and lies in the range
+    if (n_chunks == n_full || end_chunk < n_chunks) {
       phase = 2;
       return;
     }
+    next_chunk = n_full;
     B = 1;
     T = last_len;
   } else {
@@ -258,7 +272,7 @@ void dlmc_session::begin_phase() {
   rk_len.assign(B, 0);
   rk_pos.assign(B, 0);
   if (cp.schedule != DLMC_SCHED_ENTROPY) blocks = block_sizes(cp, T - std::min(cp.context, T));
-  const uint64_t end = phase == 0 ? n_full : n_chunks;
+  const uint64_t end = phase == 0 ? std::min(end_chunk, n_full) : end_chunk;
   for (int b = 0; b < B; ++b) {
     if (next_chunk < end) {
       assign(b, next_chunk++);
@@ -368,6 +382,7 @@ int dlmc_session::step(uint64_t* coded) {
         h_dec[b * mm + j] = (int32_t)v;
       }
     }
+    rk_rank.assign(h_dec, h_dec + (size_t)B * mm);
     DLMC_HIP(hipMemcpyAsync(m->dec, h_dec, (size_t)B * mm * 4, hipMemcpyHostToDevice, s));
     {
       StageTimer t(m, DLMC_STAGE_REVEAL, 0.0);
@@ -378,14 +393,22 @@ int dlmc_session::step(uint64_t* coded) {
   }
 
   const size_t row_words = (size_t)V + 1;
-  std::vector<float> Hsel;
   std::vector<int32_t> srow;
+  std::vector<float> Hall;
   if (m->trace) {
-    // the committed rows' entropies and CDFs, for the per-pass trace
+    // the committed rows' entropies (one copy of the entropies up to the
+    // highest committed row), for the per-pass trace
     srow.resize((size_t)B * mm);
     DLMC_HIP(hipMemcpy(srow.data(), m->sel_row, srow.size() * 4, hipMemcpyDeviceToHost));
+    int top = -1;
+    for (int b = 0; b < B; ++b)
+      if (slot_chunk[b] >= 0)
+        for (int j = 0; j < h_nsel[b]; ++j) top = std::max(top, srow[(size_t)b * mm + j]);
+    Hall.resize((size_t)top + 1);
+    if (top >= 0) DLMC_HIP(hipMemcpy(Hall.data(), m->H, Hall.size() * 4, hipMemcpyDeviceToHost));
   }
   bool any_dec = false;
+  std::vector<uint32_t> coded_iv;  // trace: the pass's coded pairs of one slot
   for (int b = 0; b < B; ++b) {
     if (slot_chunk[b] < 0) continue;
     const int ns = h_nsel[b];
@@ -397,12 +420,15 @@ int dlmc_session::step(uint64_t* coded) {
     }
     const uint64_t chunk = (uint64_t)slot_chunk[b];
     const uint64_t base = chunk * (uint64_t)cp.chunk_len;
-    std::vector<int32_t> syms;  // rank mode: the pass's symbols, for the trace
+    coded_iv.assign((size_t)2 * ns, 0u);
+    std::vector<int32_t> syms;  // rank mode: the pass's symbols, for the CDF-free hash
     for (int j = 0; j < ns; ++j) {
       const int pos = h_pos[b * mm + j];
       if (rank) {
         if (encode) {
           uint32_t v = h_sym[2 * (b * mm + j)];
+          coded_iv[2 * j] = v;
+          coded_iv[2 * j + 1] = h_sym[2 * (b * mm + j) + 1];
           while (v >= 0x80) {
             rk_out[b].push_back((uint8_t)(v | 0x80));
             v >>= 7;
@@ -412,9 +438,13 @@ int dlmc_session::step(uint64_t* coded) {
         } else {
           tokens[base + pos] = h_dec[b * mm + j];
           syms.push_back(h_dec[b * mm + j]);
+          coded_iv[2 * j] = (uint32_t)rk_rank[(size_t)b * mm + j];
+          coded_iv[2 * j + 1] = (uint32_t)h_dec[b * mm + j];
         }
       } else if (encode) {
         const uint32_t st = h_sym[2 * (b * mm + j)], fr = h_sym[2 * (b * mm + j) + 1];
+        coded_iv[2 * j] = st;
+        coded_iv[2 * j + 1] = fr;
         if (cp.coder == DLMC_CODER_RANS) rencs[b].encode(st, fr);
         else encs[b].encode(st, fr);
       } else {
@@ -423,16 +453,18 @@ int dlmc_session::step(uint64_t* coded) {
         if (sym < 0) throw Error(DLMC_E_CORRUPT, "decoder target out of range");
         tokens[base + pos] = sym;
         h_dec[b * mm + j] = sym;
+        coded_iv[2 * j] = cdf_j[sym];
+        coded_iv[2 * j + 1] = cdf_j[sym + 1] - cdf_j[sym];
         any_dec = true;
       }
     }
     if (m->trace) {
       std::vector<float> hv(ns);
-      for (int j = 0; j < ns; ++j)
-        DLMC_HIP(hipMemcpy(&hv[j], m->H + srow[b * mm + j], 4, hipMemcpyDeviceToHost));
+      for (int j = 0; j < ns; ++j) hv[j] = Hall[(size_t)srow[(size_t)b * mm + j]];
       const uint64_t hsh = rank ? fnv1a64(syms.data(), syms.size() * 4)
                                 : fnv1a64(rows_cdf, (size_t)ns * row_words * 4);
-      m->trace(m->trace_user, encode ? 0 : 1, chunk, slot_pass[b], ns, h_pos + b * mm, hv.data(), hsh);
+      m->trace(m->trace_user, encode ? 0 : 1, chunk, slot_pass[b], ns, h_pos + b * mm, hv.data(),
+               coded_iv.data(), hsh);
     }
     if (coded) *coded += (uint64_t)ns;
     slot_left[b] -= ns;
@@ -448,7 +480,7 @@ int dlmc_session::step(uint64_t* coded) {
   ++passes;
 
   // finished chunks: close their streams and refill their slots
-  const uint64_t end = phase == 0 ? n_full : n_chunks;
+  const uint64_t end = phase == 0 ? std::min(end_chunk, n_full) : end_chunk;
   bool base_changed = false, active = false;
   for (int b = 0; b < B; ++b) {
     if (slot_chunk[b] < 0) continue;
@@ -500,56 +532,89 @@ int dlmc_session::step(uint64_t* coded) {
   return phase == 2 ? 1 : 0;
 }
 
-std::vector<uint8_t> dlmc_session::container() const {
-  const bool crc_on = cp.flags & DLMC_FLAG_CRC;
-  const size_t hdr = FIXED_HEADER + (n_chunks + 1) * 8 + (crc_on ? n_chunks * 4 : 0);
-  // payload section: the chunk payloads back to back; the symbol ranking back
-  // end compresses the whole section as one block
+// Container layout (little endian): the 144-byte fixed header below, then
+// u64 offsets[count + 1] of the held chunks' payloads inside the payload
+// section, then (DLMC_FLAG_CRC) a u32 CRC-32 of each held chunk's tokens, then
+// the payload section -- the held chunks' payloads back to back, compressed as
+// one block for the symbol ranking back end.  A container holds the chunks
+// [first, first + count) of the input's n_chunks; it is complete when it holds
+// all of them, and only complete containers decode.
+//   0 magic, 4 version, 8 header size, 12 flags, 16 model hash, 24 seed,
+//   32 n_tokens, 40 n_chunks, 48.. codec parameters, 116 reserved (0),
+//   120 numerics id, 128 first chunk, 136 count
+static std::vector<uint8_t> fixed_header(const dlmc_model* m, const dlmc_codec_params& cp, uint64_t n,
+                                         uint64_t n_chunks) {
+  std::vector<uint8_t> h(FIXED_HEADER, 0);
+  put<uint32_t>(h, 0, MAGIC);
+  put<uint32_t>(h, 4, VERSION);
+  put<uint32_t>(h, 12, (uint32_t)cp.flags);
+  put<uint64_t>(h, 16, m->hash());
+  put<uint64_t>(h, 24, m->seed);
+  put<uint64_t>(h, 32, n);
+  put<uint64_t>(h, 40, n_chunks);
+  put<int32_t>(h, 48, cp.chunk_len);
+  put<int32_t>(h, 52, cp.cdf_bits);
+  put<int32_t>(h, 56, cp.coder_bits);
+  put<int32_t>(h, 60, cp.m_min);
+  put<int32_t>(h, 64, cp.m_max);
+  put<float>(h, 68, cp.tau_bits);
+  put<int32_t>(h, 72, cp.batch);
+  put<int32_t>(h, 76, cp.schedule);
+  put<int32_t>(h, 80, cp.blocks);
+  put<int32_t>(h, 84, cp.u1);
+  put<double>(h, 88, cp.growth);
+  put<int32_t>(h, 96, cp.coder);
+  put<int32_t>(h, 100, cp.context);
+  put<int32_t>(h, 104, cp.context_kind);
+  put<int32_t>(h, 108, cp.rank_compressor);
+  put<int32_t>(h, 112, cp.rank_level);
+  put<uint64_t>(h, 120, NUMERICS_ID);
+  return h;
+}
+
+// A container from a fixed header (fields 0..127 as above), the held range and
+// the held chunks' payloads and CRCs (crc empty unless DLMC_FLAG_CRC).
+static std::vector<uint8_t> assemble(std::vector<uint8_t> head, uint64_t first,
+                                     const std::vector<std::vector<uint8_t>>& pls,
+                                     const std::vector<uint32_t>& crc) {
+  const uint64_t cnt = pls.size();
+  const bool crc_on = get<uint32_t>(head.data(), 12) & DLMC_FLAG_CRC;
+  const int coder = get<int32_t>(head.data(), 96);
+  const size_t hdr = FIXED_HEADER + (cnt + 1) * 8 + (crc_on ? cnt * 4 : 0);
   std::vector<uint8_t> section;
-  for (const auto& p : payload) section.insert(section.end(), p.begin(), p.end());
-  if (cp.coder == DLMC_CODER_RANK) section = compress_block(cp.rank_compressor, cp.rank_level, section);
-  std::vector<uint8_t> out(hdr + section.size(), 0);
-  put<uint32_t>(out, 0, MAGIC);
-  put<uint32_t>(out, 4, VERSION);
-  put<uint32_t>(out, 8, (uint32_t)hdr);
-  put<uint32_t>(out, 12, (uint32_t)cp.flags);
-  put<uint64_t>(out, 16, m->hash());
-  put<uint64_t>(out, 24, m->seed);
-  put<uint64_t>(out, 32, n);
-  put<uint64_t>(out, 40, n_chunks);
-  put<int32_t>(out, 48, cp.chunk_len);
-  put<int32_t>(out, 52, cp.cdf_bits);
-  put<int32_t>(out, 56, cp.coder_bits);
-  put<int32_t>(out, 60, cp.m_min);
-  put<int32_t>(out, 64, cp.m_max);
-  put<float>(out, 68, cp.tau_bits);
-  put<int32_t>(out, 72, cp.batch);
-  put<int32_t>(out, 76, cp.schedule);
-  put<int32_t>(out, 80, cp.blocks);
-  put<int32_t>(out, 84, cp.u1);
-  put<double>(out, 88, cp.growth);
-  put<int32_t>(out, 96, cp.coder);
-  put<int32_t>(out, 100, cp.context);
-  put<int32_t>(out, 104, cp.context_kind);
-  put<int32_t>(out, 108, cp.rank_compressor);
-  put<int32_t>(out, 112, cp.rank_level);
+  for (const auto& p : pls) section.insert(section.end(), p.begin(), p.end());
+  if (coder == DLMC_CODER_RANK)
+    section = compress_block(get<int32_t>(head.data(), 108), get<int32_t>(head.data(), 112), section);
+  head.resize(hdr + section.size(), 0);
+  put<uint32_t>(head, 8, (uint32_t)hdr);
+  put<uint64_t>(head, 128, first);
+  put<uint64_t>(head, 136, cnt);
   uint64_t off = 0;  // offsets into the (uncompressed) payload section
-  for (uint64_t c = 0; c <= n_chunks; ++c) {
-    put<uint64_t>(out, FIXED_HEADER + c * 8, off);
-    if (c < n_chunks) off += payload[c].size();
+  for (uint64_t c = 0; c <= cnt; ++c) {
+    put<uint64_t>(head, FIXED_HEADER + c * 8, off);
+    if (c < cnt) off += pls[c].size();
   }
   if (crc_on)
-    for (uint64_t c = 0; c < n_chunks; ++c) {
+    for (uint64_t c = 0; c < cnt; ++c) put<uint32_t>(head, FIXED_HEADER + (cnt + 1) * 8 + c * 4, crc[c]);
+  if (!section.empty()) std::memcpy(head.data() + hdr, section.data(), section.size());
+  return head;
+}
+
+std::vector<uint8_t> dlmc_session::container() const {
+  std::vector<std::vector<uint8_t>> pls(payload.begin() + first_chunk, payload.begin() + end_chunk);
+  std::vector<uint32_t> crc;
+  if (cp.flags & DLMC_FLAG_CRC)
+    for (uint64_t c = first_chunk; c < end_chunk; ++c) {
       const uint64_t a = c * (uint64_t)cp.chunk_len;
       const uint64_t b = std::min<uint64_t>(n, a + cp.chunk_len);
-      put<uint32_t>(out, FIXED_HEADER + (n_chunks + 1) * 8 + c * 4,
-                    crc32(&tokens[a], (size_t)(b - a) * 4));
+      crc.push_back(crc32(&tokens[a], (size_t)(b - a) * 4));
     }
-  if (!section.empty()) std::memcpy(out.data() + hdr, section.data(), section.size());
-  return out;
+  return assemble(fixed_header(m, cp, n, n_chunks), first_chunk, pls, crc);
 }
 
 namespace dlmc {
+
+uint64_t numerics_id() { return NUMERICS_ID; }
 
 static void session_common(dlmc_session* s, dlmc_model* m, const dlmc_codec_params& cp) {
   s->m = m;
@@ -584,7 +649,7 @@ static void session_common(dlmc_session* s, dlmc_model* m, const dlmc_codec_para
 }
 
 dlmc_session* make_encoder(dlmc_model* m, const dlmc_codec_params& cp, const int32_t* tokens,
-                           uint64_t n) {
+                           uint64_t n, uint64_t first_chunk, uint64_t n_range) {
   DLMC_CHECK(tokens || n == 0, DLMC_E_INVAL, "tokens is NULL");
   for (uint64_t i = 0; i < n; ++i)
     DLMC_CHECK(tokens[i] >= 0 && tokens[i] < m->cfg.vocab, DLMC_E_INVAL,
@@ -594,6 +659,12 @@ dlmc_session* make_encoder(dlmc_model* m, const dlmc_codec_params& cp, const int
   s->n = n;
   s->tokens.assign(tokens, tokens + n);
   session_common(s.get(), m, cp);
+  if (n_range == UINT64_MAX) n_range = s->n_chunks - std::min(first_chunk, s->n_chunks);
+  DLMC_CHECK(first_chunk <= s->n_chunks && n_range <= s->n_chunks - first_chunk &&
+                 (n_range >= 1 || s->n_chunks == 0),
+             DLMC_E_INVAL, "chunk range outside the input's chunks");
+  s->first_chunk = s->next_chunk = first_chunk;
+  s->end_chunk = first_chunk + n_range;
   s->payload.assign(s->n_chunks, {});
   m->ensure_tokens(n);
   if (n) DLMC_HIP(hipMemcpyAsync(m->tokens_dev, s->tokens.data(), n * 4, hipMemcpyHostToDevice, m->stream));
@@ -601,16 +672,21 @@ dlmc_session* make_encoder(dlmc_model* m, const dlmc_codec_params& cp, const int
   return s.release();
 }
 
-void parse_header(const uint8_t* in, uint64_t len, dlmc_codec_params* cp, uint64_t* n,
-                  uint64_t* n_chunks, uint64_t* hash, uint64_t* seed, uint32_t* hdr) {
+void parse_header(const uint8_t* in, uint64_t len, ContainerInfo* ci) {
   DLMC_CHECK(in && len >= FIXED_HEADER, DLMC_E_FORMAT, "container too short");
   DLMC_CHECK(get<uint32_t>(in, 0) == MAGIC, DLMC_E_FORMAT, "bad magic");
   DLMC_CHECK(get<uint32_t>(in, 4) == VERSION, DLMC_E_FORMAT, "unsupported container version");
-  *hdr = get<uint32_t>(in, 8);
-  *hash = get<uint64_t>(in, 16);
-  *seed = get<uint64_t>(in, 24);
-  *n = get<uint64_t>(in, 32);
-  *n_chunks = get<uint64_t>(in, 40);
+  DLMC_CHECK(get<uint64_t>(in, 120) == NUMERICS_ID, DLMC_E_FORMAT,
+             "container was made by a build with other kernel arithmetic (numerics id mismatch)");
+  dlmc_codec_params* cp = &ci->cp;
+  *cp = dlmc_codec_params{};
+  ci->hdr = get<uint32_t>(in, 8);
+  ci->hash = get<uint64_t>(in, 16);
+  ci->seed = get<uint64_t>(in, 24);
+  ci->n = get<uint64_t>(in, 32);
+  ci->n_chunks = get<uint64_t>(in, 40);
+  ci->first = get<uint64_t>(in, 128);
+  ci->count = get<uint64_t>(in, 136);
   cp->struct_size = sizeof(dlmc_codec_params);
   cp->flags = (int32_t)get<uint32_t>(in, 12);
   cp->chunk_len = get<int32_t>(in, 48);
@@ -632,55 +708,103 @@ void parse_header(const uint8_t* in, uint64_t len, dlmc_codec_params* cp, uint64
   cp->reserved = 0;
   cp->context_seed = 0;  // positions are stored with each chunk
   DLMC_CHECK(cp->chunk_len >= 1, DLMC_E_FORMAT, "bad chunk length");
-  DLMC_CHECK(*n_chunks == (*n + cp->chunk_len - 1) / cp->chunk_len, DLMC_E_FORMAT, "bad chunk count");
+  DLMC_CHECK(ci->n_chunks == (ci->n + cp->chunk_len - 1) / cp->chunk_len, DLMC_E_FORMAT, "bad chunk count");
+  DLMC_CHECK(ci->first <= ci->n_chunks && ci->count <= ci->n_chunks - ci->first &&
+                 (ci->count >= 1 || ci->n_chunks == 0),
+             DLMC_E_FORMAT, "bad chunk range");
   const bool crc_on = cp->flags & DLMC_FLAG_CRC;
-  const uint64_t need = FIXED_HEADER + (*n_chunks + 1) * 8 + (crc_on ? *n_chunks * 4 : 0);
-  DLMC_CHECK(*hdr == need && len >= need, DLMC_E_FORMAT, "bad header size");
+  const uint64_t need = FIXED_HEADER + (ci->count + 1) * 8 + (crc_on ? ci->count * 4 : 0);
+  DLMC_CHECK(ci->hdr == need && len >= need, DLMC_E_FORMAT, "bad header size");
+  DLMC_CHECK(get<uint64_t>(in, FIXED_HEADER) == 0, DLMC_E_FORMAT, "bad chunk offsets");
+  ci->total = get<uint64_t>(in, FIXED_HEADER + ci->count * 8);
 }
 
-dlmc_session* make_decoder(dlmc_model* m, const uint8_t* in, uint64_t len, int32_t batch) {
-  dlmc_codec_params cp{};
-  uint64_t n, nc, hash, seed;
-  uint32_t hdr;
-  parse_header(in, len, &cp, &n, &nc, &hash, &seed, &hdr);
-  DLMC_CHECK(hash == m->hash(), DLMC_E_FORMAT, "container was made by another model or seed");
-  if (batch > 0) cp.batch = batch;
-  cp.batch = std::min(cp.batch, m->cfg.max_batch);
-  std::unique_ptr<dlmc_session> s(new dlmc_session());
-  s->encode = false;
-  s->n = n;
-  session_common(s.get(), m, cp);
-  s->tokens.assign(n, 0);
-  s->payload.resize(nc);
-  s->crc.resize(nc);
-  const uint64_t total = get<uint64_t>(in, FIXED_HEADER + nc * 8);
-  DLMC_CHECK(get<uint64_t>(in, FIXED_HEADER) == 0, DLMC_E_FORMAT, "bad chunk offsets");
+// The held chunks' payloads of a parsed container (the payload section
+// decompressed for the symbol ranking back end), and their CRCs.
+static void read_payloads(const uint8_t* in, uint64_t len, const ContainerInfo& ci,
+                          std::vector<std::vector<uint8_t>>& pls, std::vector<uint32_t>& crc) {
+  const uint64_t nc = ci.count;
   std::vector<uint8_t> unpacked;
-  const uint8_t* section = in + hdr;
-  if (cp.coder == DLMC_CODER_RANK) {
+  const uint8_t* section = in + ci.hdr;
+  if (ci.cp.coder == DLMC_CODER_RANK) {
     // context and varint ranks take at most 11 bytes a token
-    DLMC_CHECK(total <= 16 * n + 1024, DLMC_E_FORMAT, "bad payload size");
-    unpacked = decompress_block(cp.rank_compressor, in + hdr, len - hdr, total);
+    DLMC_CHECK(ci.total <= 16 * ci.n + 1024, DLMC_E_FORMAT, "bad payload size");
+    unpacked = decompress_block(ci.cp.rank_compressor, in + ci.hdr, len - ci.hdr, ci.total);
     section = unpacked.data();
   } else {
-    DLMC_CHECK(hdr + total <= len, DLMC_E_FORMAT, "bad chunk offsets");
+    DLMC_CHECK(ci.hdr + ci.total <= len, DLMC_E_FORMAT, "bad chunk offsets");
   }
+  pls.assign(nc, {});
+  crc.assign((ci.cp.flags & DLMC_FLAG_CRC) ? nc : 0, 0u);
   uint64_t prev = 0;
   for (uint64_t c = 0; c < nc; ++c) {
     const uint64_t a = get<uint64_t>(in, FIXED_HEADER + c * 8);
     const uint64_t b = get<uint64_t>(in, FIXED_HEADER + (c + 1) * 8);
-    DLMC_CHECK(a == prev && b >= a && b <= total, DLMC_E_FORMAT, "bad chunk offsets");
-    s->payload[c].assign(section + a, section + b);
+    DLMC_CHECK(a == prev && b >= a && b <= ci.total, DLMC_E_FORMAT, "bad chunk offsets");
+    pls[c].assign(section + a, section + b);
     prev = b;
-    if (cp.flags & DLMC_FLAG_CRC) s->crc[c] = get<uint32_t>(in, FIXED_HEADER + (nc + 1) * 8 + c * 4);
+    if (ci.cp.flags & DLMC_FLAG_CRC) crc[c] = get<uint32_t>(in, FIXED_HEADER + (nc + 1) * 8 + c * 4);
   }
+}
+
+dlmc_session* make_decoder(dlmc_model* m, const uint8_t* in, uint64_t len, int32_t batch) {
+  ContainerInfo ci;
+  parse_header(in, len, &ci);
+  DLMC_CHECK(ci.hash == m->hash(), DLMC_E_FORMAT, "container was made by another model or seed");
+  DLMC_CHECK(ci.first == 0 && ci.count == ci.n_chunks, DLMC_E_FORMAT,
+             "partial container (a chunk range): merge the parts first");
+  dlmc_codec_params cp = ci.cp;
+  if (batch > 0) cp.batch = batch;
+  cp.batch = std::min(cp.batch, m->cfg.max_batch);
+  std::unique_ptr<dlmc_session> s(new dlmc_session());
+  s->encode = false;
+  s->n = ci.n;
+  session_common(s.get(), m, cp);
+  s->first_chunk = s->next_chunk = 0;
+  s->end_chunk = ci.n_chunks;
+  s->tokens.assign(ci.n, 0);
+  read_payloads(in, len, ci, s->payload, s->crc);
   return s.release();
 }
 
-uint64_t encode_bound(const dlmc_codec_params& cp, uint64_t n) {
-  const uint64_t nc = (n + cp.chunk_len - 1) / cp.chunk_len;
-  uint64_t total = FIXED_HEADER + (nc + 1) * 8 + ((cp.flags & DLMC_FLAG_CRC) ? nc * 4 : 0);
-  for (uint64_t c = 0; c < nc; ++c) {
+std::vector<uint8_t> merge_containers(const uint8_t* const* parts, const uint64_t* lens, int n_parts) {
+  DLMC_CHECK(n_parts >= 1 && parts && lens, DLMC_E_INVAL, "no containers to merge");
+  std::vector<ContainerInfo> info(n_parts);
+  std::vector<int> order(n_parts);
+  for (int i = 0; i < n_parts; ++i) {
+    DLMC_CHECK(parts[i], DLMC_E_INVAL, "NULL container");
+    parse_header(parts[i], lens[i], &info[i]);
+    // every header field but the size and the chunk range must agree
+    DLMC_CHECK(std::memcmp(parts[i], parts[0], 8) == 0 && std::memcmp(parts[i] + 12, parts[0] + 12, 116) == 0,
+               DLMC_E_FORMAT, "containers of different inputs, models or codec parameters");
+    order[i] = i;
+  }
+  std::sort(order.begin(), order.end(), [&](int a, int b) { return info[a].first < info[b].first; });
+  std::vector<std::vector<uint8_t>> pls;
+  std::vector<uint32_t> crc;
+  uint64_t next = 0;
+  for (int i : order) {
+    DLMC_CHECK(info[i].first == next, DLMC_E_FORMAT, "chunk ranges overlap or leave a gap");
+    std::vector<std::vector<uint8_t>> p;
+    std::vector<uint32_t> c;
+    read_payloads(parts[i], lens[i], info[i], p, c);
+    for (auto& x : p) pls.push_back(std::move(x));
+    crc.insert(crc.end(), c.begin(), c.end());
+    next += info[i].count;
+  }
+  DLMC_CHECK(next == info[0].n_chunks, DLMC_E_FORMAT, "the containers do not hold every chunk");
+  std::vector<uint8_t> head(parts[0], parts[0] + 128);
+  head.resize(FIXED_HEADER, 0);
+  return assemble(std::move(head), 0, pls, crc);
+}
+
+uint64_t encode_bound(const dlmc_codec_params& cp, uint64_t n, uint64_t first, uint64_t count) {
+  const uint64_t nc_all = (n + cp.chunk_len - 1) / cp.chunk_len;
+  if (first > nc_all) first = nc_all;
+  if (count > nc_all - first) count = nc_all - first;
+  const uint64_t head = FIXED_HEADER + (count + 1) * 8 + ((cp.flags & DLMC_FLAG_CRC) ? count * 4 : 0);
+  uint64_t total = head;
+  for (uint64_t c = first; c < first + count; ++c) {
     const uint64_t len = std::min<uint64_t>(cp.chunk_len, n - c * cp.chunk_len);
     const uint64_t ctx = std::min<uint64_t>((uint64_t)cp.context, len);
     const uint64_t coded = len - ctx;
@@ -692,11 +816,7 @@ uint64_t encode_bound(const dlmc_codec_params& cp, uint64_t n) {
     else
       total += (coded * (cp.cdf_bits + 1) + 7) / 8 + cp.coder_bits / 8 + 2;
   }
-  if (cp.coder == DLMC_CODER_RANK) {
-    // room for a compressor's worst case on incompressible input
-    const uint64_t body = total - (FIXED_HEADER + (nc + 1) * 8 + ((cp.flags & DLMC_FLAG_CRC) ? nc * 4 : 0));
-    total += body / 128 + 1024;
-  }
+  if (cp.coder == DLMC_CODER_RANK) total += (total - head) / 128 + 1024;  // a compressor's worst case
   return total;
 }
 

@@ -39,13 +39,13 @@ def rel_err_rows(gpu, ref):
     return float((num / den).max())
 
 
-FIXED_HEADER = 120  # container version 2
+FIXED_HEADER = 144  # container version 3
 
 
 def payloads(container: bytes):
-    """Per-chunk payloads of a dlmc container (layout of include/dlmc.h)."""
+    """Per-chunk payloads held by a dlmc container (layout of include/dlmc.h)."""
     hdr = int.from_bytes(container[8:12], "little")
-    nc = int.from_bytes(container[40:48], "little")
+    nc = int.from_bytes(container[136:144], "little")
     offs = [int.from_bytes(container[FIXED_HEADER + 8 * c: FIXED_HEADER + 8 + 8 * c], "little")
             for c in range(nc + 1)]
     return [container[hdr + offs[c]: hdr + offs[c + 1]] for c in range(nc)]

@@ -30,24 +30,32 @@ def dev_state(st):
     return torch.from_numpy(np.ascontiguousarray(st, dtype=np.int32)).cuda()
 
 
-def roundtrip_workload(name, n_chunks, batch=None, max_seconds=None):
+def roundtrip_workload(name, n_chunks, batch=None, trace=False):
+    """Round trip of the first n_chunks chunks of a workload.  With trace, the
+    per-pass decisions of encode and decode (positions, entropies, coded
+    intervals, CDF hashes) must be identical."""
     w = wl.WORKLOADS[name]
     cd = w.codec if batch is None else dataclasses.replace(w.codec, batch=batch)
     toks = wl.make_tokens(w, n_chunks * cd.chunk_len)
     log("round trip", name, f"{n_chunks} chunks x {cd.chunk_len}, batch {cd.batch}")
-    passes = {}
+    traces = {0: {}, 1: {}}
 
-    def tr(d, chunk, pas, pos, ent, h):
-        if d == 0:
-            passes[chunk] = max(passes.get(chunk, 0), pas + 1)
+    def tr(d, chunk, pas, pos, ent, coded, h):
+        traces[d][(chunk, pas)] = (tuple(pos), tuple(ent), tuple(coded), h)
 
     with dl.Model(w.model, max_chunk=cd.chunk_len, max_batch=cd.batch) as m:
+        if trace:
+            m.set_trace(tr, coded=True)
         t0 = time.time()
         data = m.encode(toks, cd)
         t1 = time.time()
         back = m.decode(data)
         t2 = time.time()
+        m.set_trace(None)
     assert np.array_equal(back, toks)
+    if trace:
+        assert len(traces[0]) > 0 and traces[0] == traces[1]
+        log(f"{name}: encode and decode traces identical over {len(traces[0])} (chunk, pass) records")
     log(f"{name}: {len(toks)} tokens -> {len(data)} bytes "
         f"({8 * len(data) / (len(toks) * w.token_bytes):.3f} bits/input byte), "
         f"encode {t1 - t0:.1f}s decode {t2 - t1:.1f}s")
@@ -59,7 +67,7 @@ def test_roundtrip_small_config():
 
 
 def test_roundtrip_8b_config():
-    roundtrip_workload("8b", 1)
+    roundtrip_workload("8b", 1, trace=True)
 
 
 def test_roundtrip_8b_threshold_schedule():
@@ -67,20 +75,27 @@ def test_roundtrip_8b_threshold_schedule():
     w = wl.WORKLOADS["8b-throughput"]
     cd = dataclasses.replace(w.codec, batch=2)
     toks = wl.make_tokens(w, 2 * cd.chunk_len)
-    counts = []
+    traces = {0: {}, 1: {}}
 
-    def tr(d, chunk, pas, pos, ent, h):
-        if d == 0:
-            counts.append((chunk, len(pos)))
+    def tr(d, chunk, pas, pos, ent, coded, h):
+        traces[d][(chunk, pas)] = (tuple(pos), tuple(ent), tuple(coded), h)
 
     with dl.Model(w.model, max_chunk=cd.chunk_len, max_batch=2) as m:
-        m.set_trace(tr)
+        m.set_trace(tr, coded=True)
         data = m.encode(toks, cd)
-        m.set_trace(None)
         back = m.decode(data)
+        m.set_trace(None)
     assert np.array_equal(back, toks)
+    # encode and decode took bit-identical decisions under the 0.5-bit rule
+    assert traces[0] == traces[1]
+    counts = [(c, len(t[0])) for (c, _), t in traces[0].items()]
     per_chunk = [sum(1 for c, _ in counts if c == k) for k in range(2)]
     assert all(1 <= n <= 64 for _, n in counts)
+    # every pass commits all positions at or under 0.5 bits (capped at 64),
+    # at least one
+    for t in traces[0].values():
+        ent = t[1]
+        assert sum(h <= 0.5 for h in ent) == len(ent) or len(ent) == 1 or len(ent) == 64
     log("8b-throughput passes per chunk", per_chunk)
 
 
@@ -103,6 +118,29 @@ def test_logits_8b_full_width_one_layer():
     ref, pos = OM.logits(sh, W, st[0], vocab_rows=cols)
     assert np.array_equal(rows, pos)
     err = rel_err_rows(gpu, ref)
+    log("max rel err", err)
+    assert err <= 2e-2
+
+
+@pytest.mark.timeout(400)  # the fp64 oracle takes about a minute at T = 8192
+def test_logits_8b_long_attention_launch():
+    """The long-chunk workload's attention launch: d_model 4096, 32 heads of
+    128, one chunk of 8192 (with four chunks the workload runs the same
+    blocks): (8192 / 256) x 32 = 1024 blocks, so attention runs 256-query
+    blocks.  One layer, a small FFN and vocabulary keep the fp64 oracle
+    affordable; QKV, attention and O-proj run at the workload's shape."""
+    sh = dataclasses.replace(wl.with_layers(wl.DLM8B, 1), d_ffn=512, vocab=384,
+                             ffn_out_exp=wl.fan_in_exp(512))
+    T = 8192
+    st = wl.random_state(23, 1, T, sh.vocab, 0.3)
+    log("8b-long attention launch: L=1 d=4096 32x128 T=8192")
+    with dl.Model(sh, max_chunk=T, max_batch=1) as m:
+        lg, rows = m.forward_logits(dev_state(st))
+        lg, rows = lg.cpu().numpy(), rows.cpu().numpy()
+    log("oracle (fp64) forward at T=8192")
+    ref, pos = OM.logits(sh, OW.Weights(sh), st[0])
+    assert np.array_equal(rows, pos)
+    err = rel_err_rows(lg, ref)
     log("max rel err", err)
     assert err <= 2e-2
 

@@ -250,30 +250,104 @@ def roundtrip(m, toks, cd, batch_dec=0, crc=False):
     return data
 
 
+def coded_bits(pairs, P):
+    """sum -log2(f / 2^P) over coded (start, f) pairs: the information content
+    of the symbols under the quantised distributions actually coded."""
+    return float(sum(P - math.log2(f) for _, f in pairs))
+
+
+def trace_recorder():
+    traces = {0: {}, 1: {}}
+
+    def tr(d, chunk, pas, pos, ent, coded, h):
+        traces[d][(chunk, pas)] = (tuple(pos), tuple(ent), tuple(coded), h)
+
+    return traces, tr
+
+
 def test_roundtrip_tiny_workload_full_with_trace_and_code_length():
+    """fp32 tiny model, the whole 4 KiB input: encode and decode take
+    bit-identical decisions; along the GPU's own trajectory the code length
+    sum -log2 q of the coded symbols is within 0.5% of the oracle's (no
+    additive slack); and the GPU payload is exactly what the oracle's range
+    coder writes for the GPU's coded intervals."""
+    from oracle import coder as ORC
     w = wl.WORKLOADS["tiny"]
     toks = wl.make_tokens(w)
     log("tiny round trip", len(toks))
-    traces = {0: {}, 1: {}}
-
-    def tr(d, chunk, pas, pos, ent, h):
-        traces[d][(chunk, pas)] = (tuple(pos), tuple(ent), h)
-
+    traces, tr = trace_recorder()
     with dl.Model(w.model, max_chunk=w.codec.chunk_len, max_batch=w.codec.batch) as m:
-        m.set_trace(tr)
+        m.set_trace(tr, coded=True)
         data = roundtrip(m, toks, w.codec)
         m.set_trace(None)
-    # encode and decode made bit-identical decisions and CDFs
+    # encode and decode made bit-identical decisions, CDFs and coded intervals
     assert traces[0] == traces[1] and len(traces[0]) == 16 * 64
-    # code length against the oracle replaying the GPU's trajectory
     W = OW.Weights(w.model)
-    gpu_bytes = [len(p) for p in payloads(data)]
+    P, Wc = w.codec.cdf_bits, w.codec.coder_bits
+    gpu_payloads = payloads(data)
     for c in (0, 7):
-        forced = [np.array(traces[0][(c, p)][0]) for p in range(64)]
+        passes = [traces[0][(c, p)] for p in range(64)]
+        pairs = [iv for t in passes for iv in t[2]]
+        enc = ORC.RangeEncoder(Wc, P)
+        for st, f in pairs:
+            enc.encode(st, f)
+        assert enc.finish() == gpu_payloads[c]
+        forced = [np.array(t[0]) for t in passes]
         seg = toks[c * 256:(c + 1) * 256]
         r = OD.encode_chunk(w.model, W, seg, w.codec, forced=forced)
-        assert abs(gpu_bytes[c] - len(r.payload)) / len(r.payload) <= 0.005 + 4.0 / len(r.payload)
-        assert abs(gpu_bytes[c] * 8 - 32 - r.coded_bits) / r.coded_bits <= 0.005 + 16 / r.coded_bits
+        gpu_bits = coded_bits(pairs, P)
+        rel = abs(gpu_bits - r.ideal_bits) / r.ideal_bits
+        log(f"tiny chunk {c}: code length {gpu_bits:.3f} vs oracle {r.ideal_bits:.3f} bits, rel {rel:.2e}")
+        assert rel <= 0.005
+
+
+def oracle_bits_along(sh, W, toks, enc_passes, P, sample):
+    """sum -log2 q under the oracle's fp64 CDFs of the symbols the GPU coded in
+    the sampled passes, each pass evaluated at the state the GPU's earlier
+    selections leave (the GPU's trajectory)."""
+    from oracle import cdf as OCdf
+    T = len(toks)
+    bits = 0.0
+    for p in sample:
+        state = np.full(T, sh.mask_id, dtype=np.int64)
+        for q in range(p):
+            sel = np.array(enc_passes[q][0], dtype=np.int64)
+            state[sel] = toks[sel]
+        lg, pos = OM.logits(sh, W, state)
+        row_of = {int(x): i for i, x in enumerate(pos)}
+        for x in enc_passes[p][0]:
+            cdf = OCdf.cdf_row(lg[row_of[int(x)]], P)
+            s_ = int(toks[x])
+            bits += P - math.log2(int(cdf[s_ + 1] - cdf[s_]))
+    return bits
+
+
+def test_code_length_bf16_small_shape_two_layers():
+    """The small model's shape (d 768, 12 heads, GELU 3072, vocabulary 32768)
+    with 2 layers, bf16, one 1024-token chunk, k = 8, P = 24, W = 64: encode
+    and decode traces are identical, and over every eighth pass (16 passes,
+    128 symbols) the GPU's sum -log2 q is within 0.5% of the oracle's fp64
+    value along the GPU's trajectory, with no additive slack."""
+    w = wl.WORKLOADS["small"]
+    sh = wl.with_layers(w.model, 2)
+    cd = w.codec
+    toks = wl.make_tokens(w, cd.chunk_len)
+    log("bf16 code length", sh.name, cd)
+    traces, tr = trace_recorder()
+    with dl.Model(sh, max_chunk=cd.chunk_len, max_batch=1) as m:
+        m.set_trace(tr, coded=True)
+        data = m.encode(toks, cd, batch=1)
+        back = m.decode(data)
+        m.set_trace(None)
+    assert np.array_equal(back, toks)
+    assert traces[0] == traces[1] and len(traces[0]) == cd.chunk_len // cd.m_max
+    enc = [traces[0][(0, p)] for p in range(len(traces[0]))]
+    sample = list(range(0, len(enc), 8))
+    gpu_bits = sum(coded_bits(enc[p][2], cd.cdf_bits) for p in sample)
+    ref_bits = oracle_bits_along(sh, OW.Weights(sh), toks, enc, cd.cdf_bits, sample)
+    rel = abs(gpu_bits - ref_bits) / ref_bits
+    log(f"bf16 small L=2: code length {gpu_bits:.2f} vs oracle {ref_bits:.2f} bits, rel {rel:.2e}")
+    assert rel <= 0.005
 
 
 @pytest.mark.parametrize("dec_batch", [1, 3])
@@ -380,3 +454,80 @@ def test_stage_profile_mask():
         p = m.profile_read()
         assert p["ffn_in"][1] == 3 and p["head"][1] == 3 and p["qkv"][1] == 0
         m.profile(False)
+
+
+# ---------------------------------------------------------------- error codes
+def test_numeric_errors():
+    """E_NUMERIC: the schedule refuses non-finite entropies, and the encoder
+    refuses a pass whose model output holds a NaN (forced by the test hook);
+    the model keeps working afterwards."""
+    sh = shape(vocab=10, n_layers=0)
+    rows = np.arange(8, dtype=np.int32)
+    H = np.linspace(0.5, 3.0, 8).astype(np.float32)
+    H[5] = np.nan
+    with dl.Model(sh, max_chunk=16) as m:
+        with pytest.raises(dl.DlmcError) as e:
+            m.select(torch.from_numpy(H).cuda(), torch.from_numpy(rows).cuda(), 1, 16,
+                     float("-inf"), 2, 2)
+        assert e.value.code == -7
+        H[5] = np.inf
+        with pytest.raises(dl.DlmcError) as e:
+            m.select(torch.from_numpy(H).cuda(), torch.from_numpy(rows).cuda(), 1, 16, 1.0, 1, 4)
+        assert e.value.code == -7
+    sh = shape()
+    cd = codec(32, k=4)
+    toks = wl.markov1_tokens(70, sh.vocab, 3)
+    with dl.Model(sh, max_chunk=32) as m:
+        m.inject_nonfinite(True)
+        with pytest.raises(dl.DlmcError) as e:
+            m.encode(toks, cd)
+        assert e.value.code == -7
+        m.inject_nonfinite(False)
+        assert np.array_equal(m.decode(m.encode(toks, cd)), toks)
+
+
+def test_out_of_memory_is_reported():
+    """E_NOMEM: a workspace for 128 chunks of 8192 tokens over a 126464-symbol
+    vocabulary needs 530 GB of fp32 logits; the model is refused before any
+    kernel runs, and the GPU stays usable."""
+    big = shape(n_layers=0, vocab=126464)
+    with pytest.raises(dl.DlmcError) as e:
+        dl.Model(big, max_chunk=8192, max_batch=128)
+    assert e.value.code == -2
+    sh = shape()
+    toks = wl.markov1_tokens(40, sh.vocab, 5)
+    with dl.Model(sh, max_chunk=32) as m:
+        assert np.array_equal(m.decode(m.encode(toks, codec(32, k=4))), toks)
+
+
+# ---------------------------------------------------------------- chunk ranges
+@pytest.mark.parametrize("kw", [
+    dict(k=5),
+    dict(mmin=1, mmax=16, schedule="uniform", blocks=8, coder="rank", rank_compressor="zlib",
+         rank_level=6),
+    dict(k=4, coder="rans", context=3, context_kind="random", context_seed=2),
+])
+def test_encode_range_and_merge_byte_identical(kw):
+    """Chunks [0, 2) coded by one model handle and [2, 6) by another (the last
+    chunk partial), merged: byte-identical to one encode of the whole input
+    (windows are independent), and the merged container decodes.  A partial
+    container does not decode on its own."""
+    sh = shape(ffn="swiglu", norm="rmsnorm")
+    cd = codec(64, P=24, W=64, batch=2, **kw)
+    toks = wl.markov1_tokens(64 * 5 + 23, sh.vocab, 17)
+    log("encode range + merge", kw)
+    with dl.Model(sh, max_chunk=64, max_batch=2) as m1, dl.Model(sh, max_chunk=64, max_batch=2) as m2:
+        full = m1.encode(toks, cd, crc=True)
+        a = m1.encode_range(toks, cd, 0, 2, crc=True)
+        b = m2.encode_range(toks, cd, 2, 4, crc=True)
+        assert dl.merge([b, a]) == full
+        c = m2.encode_range(toks, cd, 3, 2 ** 64 - 1, crc=True)           # to the last chunk
+        mid = m1.encode_range(toks, cd, 2, 1, crc=True)
+        assert dl.merge([a, mid, c]) == full
+        assert np.array_equal(m2.decode(dl.merge([a, b]), batch=1), toks)
+        with pytest.raises(dl.DlmcError) as e:
+            m1.decode(a)
+        assert e.value.code == -4
+        with pytest.raises(dl.DlmcError) as e:
+            m1.encode_range(toks, cd, 5, 2)
+        assert e.value.code == -1

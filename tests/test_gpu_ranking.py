@@ -53,7 +53,7 @@ def test_rank_and_select_kernels_exact(V):
 
 def section(container: bytes, kind: str):
     hdr = int.from_bytes(container[8:12], "little")
-    nc = int.from_bytes(container[40:48], "little")
+    nc = int.from_bytes(container[136:144], "little")
     offs = [int.from_bytes(container[FIXED_HEADER + 8 * c: FIXED_HEADER + 8 + 8 * c], "little")
             for c in range(nc + 1)]
     body = R.decompress(container[hdr:], kind)

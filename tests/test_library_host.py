@@ -123,3 +123,95 @@ def test_host_rans_rejects_bad_input():
         with pytest.raises(dl.DlmcError) as e:
             dl.rans_decode(bad, cdf, 16)
         assert e.value.code == -5
+
+
+# ---------------------------------------------------------------- container header
+def make_container(payloads, n_tokens, chunk_len, first=0, count=None, numerics=None, crc=None,
+                   flags=0, seed=7, tau=float("-inf")):
+    """A version-3 container written field by field from the layout that
+    include/dlmc.h documents (range coder, so the payload section is stored
+    as is)."""
+    import struct
+    n_chunks = -(-n_tokens // chunk_len)
+    count = len(payloads) if count is None else count
+    numerics = dl.numerics_id() if numerics is None else numerics
+    if crc is not None:
+        flags |= 1
+    fixed = bytearray(144)
+    struct.pack_into("<IIII", fixed, 0, 0x434D4C44, 3, 0, flags)
+    struct.pack_into("<QQQQ", fixed, 16, 0x1234, seed, n_tokens, n_chunks)
+    struct.pack_into("<iiiiifiiii", fixed, 48, chunk_len, 16, 32, 4, 4, tau, 1, 0, 0, 0)
+    struct.pack_into("<d", fixed, 88, 1.0)
+    struct.pack_into("<iiiiiI", fixed, 96, 0, 0, 0, 0, 0, 0)
+    struct.pack_into("<QQQ", fixed, 120, numerics, first, count)
+    offs = [0]
+    for p in payloads:
+        offs.append(offs[-1] + len(p))
+    tail = b"".join(struct.pack("<Q", o) for o in offs)
+    if crc is not None:
+        tail += b"".join(struct.pack("<I", c) for c in crc)
+    hdr = 144 + len(tail)
+    struct.pack_into("<I", fixed, 8, hdr)
+    return bytes(fixed) + tail + b"".join(payloads)
+
+
+def test_numerics_id_is_recorded_and_checked():
+    """A container made by a build with other kernel arithmetic must be
+    refused at the header: the decoder could not replay its decisions."""
+    nid = dl.numerics_id()
+    assert nid != 0
+    good = make_container([b"\x01\x02", b"\x03"], 10, 5)
+    assert dl.decode_size(good) == 10
+    bad = make_container([b"\x01\x02", b"\x03"], 10, 5, numerics=nid ^ 1)
+    with pytest.raises(dl.DlmcError) as e:
+        dl.decode_size(bad)
+    assert e.value.code == -4 and "numerics" in str(e.value)
+
+
+def test_header_rejects_bad_ranges_and_sizes():
+    good = make_container([b"ab", b"c", b"d"], 11, 4)
+    assert dl.decode_size(good) == 11
+    for bad in (make_container([b"ab"], 11, 4, first=3),          # past the last chunk
+                make_container([b"a", b"b"], 11, 4, first=2),      # runs past the last chunk
+                make_container([], 11, 4),                          # holds nothing
+                good[:150]):                                        # offsets cut short
+        with pytest.raises(dl.DlmcError) as e:
+            dl.decode_size(bad)
+        assert e.value.code == -4
+    doctored = bytearray(good)
+    doctored[8] ^= 8                                                # header size
+    with pytest.raises(dl.DlmcError) as e:
+        dl.decode_size(bytes(doctored))
+    assert e.value.code == -4
+
+
+def test_merge_reassembles_the_complete_container():
+    pls = [b"p0-x", b"p1", b"", b"p3-yyy", b"p4"]
+    crc = [11, 22, 33, 44, 55]
+    full = make_container(pls, 5 * 8 - 3, 8, crc=crc)
+    a = make_container(pls[:2], 37, 8, first=0, crc=crc[:2])
+    b = make_container(pls[2:4], 37, 8, first=2, crc=crc[2:4])
+    c = make_container(pls[4:], 37, 8, first=4, crc=crc[4:])
+    assert dl.merge([a, b, c]) == full
+    assert dl.merge([c, a, b]) == full                               # any order
+    assert dl.merge([full]) == full
+    assert dl.merge([a, make_container(pls[2:], 37, 8, first=2, crc=crc[2:])]) == full
+
+
+@pytest.mark.parametrize("case", ["gap", "overlap", "missing", "codec", "numerics", "n_tokens"])
+def test_merge_rejects_parts_that_do_not_tile(case):
+    pls = [b"aa", b"bb", b"cc"]
+    a = make_container(pls[:1], 24, 8, first=0)
+    b = make_container(pls[1:2], 24, 8, first=1)
+    c = make_container(pls[2:], 24, 8, first=2)
+    parts = {
+        "gap": [a, c],
+        "overlap": [a, make_container(pls[:2], 24, 8, first=0), b, c],
+        "missing": [a, b],
+        "codec": [a, b, make_container(pls[2:], 24, 8, first=2, tau=0.5)],
+        "numerics": [a, b, make_container(pls[2:], 24, 8, first=2, numerics=dl.numerics_id() ^ 2)],
+        "n_tokens": [a, b, make_container(pls[2:], 23, 8, first=2)],
+    }[case]
+    with pytest.raises(dl.DlmcError) as e:
+        dl.merge(parts)
+    assert e.value.code == -4, case
