@@ -85,7 +85,8 @@ def cpu_baseline(w, layers_timed=1, vocab_sample=4096):
     return {
         "value": k * w.token_bytes / t_pass,
         "unit": "B/s",
-        "cores": threads,
+        "cores": threads,              # BLAS threads the oracle ran on
+        "host_cpus": os.cpu_count(),   # logical CPUs of the host
         "kind": "oracle",
         "sample": (f"one pass of one {T}-token chunk, {T // 2} masked: {layers_timed} of "
                    f"{sh.n_layers} layers timed (x{sh.n_layers}), LM head on a {vs}-row vocab "
@@ -293,6 +294,14 @@ def main():
             "unit": "TFLOP/s",
             "frac": round(achieved / peak, 4),
             "traffic": measured_traffic() if (dom == "ffn_in" and args.workload == "8b") else None,
+            # the whole step: the algorithmic flops of one pass (every layer
+            # GEMM and attention, the LM head at the masked rows, averaged over
+            # the timed passes) over the measured time per step
+            "step": {
+                "flops_per_step": step_flops,
+                "achieved": round(step_flops / (elapsed / steps) / 1e12, 1),
+                "frac": round(step_flops / (elapsed / steps) / 1e12 / peak, 4),
+            },
         },
         "detail": {
             "tokens_per_s": coded / elapsed,
