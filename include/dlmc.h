@@ -274,6 +274,23 @@ dlmc_status dlmc_forward_logits(dlmc_model* model, const int32_t* state, int32_t
 dlmc_status dlmc_entropy_cdf(dlmc_model* model, const float* logits, int32_t n_rows,
                              int32_t cdf_bits, float* entropy_bits, float* row_max,
                              uint32_t* g, uint32_t* cdf);
+/* dlmc_entropy_cdf for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  Same arguments and results, bit for bit; no hipMalloc,
+ * hipFree or other allocating call: the CDF's per-row tables and segment
+ * partials live in the library's static device scratch of DLMC_SCRATCH_BYTES
+ * per GPU (held by each GPU the library runs on until the process ends),
+ * which must hold 8 n_rows bytes rounded up to 256 plus
+ * 20 n_rows ceil(vocab / 4096) bytes when a CDF is asked for (about 6600
+ * rows at vocab 126464); larger requests fail with E_INVAL before any work.
+ * Asynchronous: the results are complete when the model's stream
+ * (dlmc_set_stream) reaches the end of the call's work.  Every call on a GPU
+ * shares that GPU's scratch, so calls that overlap in time on one GPU (other
+ * streams, other host threads, other model handles) race: serialise them. */
+#define DLMC_SCRATCH_BYTES (4u << 20)
+dlmc_status dlmc_entropy_cdf_noalloc(dlmc_model* model, const float* logits, int32_t n_rows,
+                                     int32_t cdf_bits, float* entropy_bits, float* row_max,
+                                     uint32_t* g, uint32_t* cdf);
 /* The commitment schedule on device entropies: rows[n_rows] are flat b*T+t
  * indices ascending (as from dlmc_forward_logits) with entropies H[n_rows].
  * Writes per chunk b the committed positions sel_pos[b*m_max + j], their

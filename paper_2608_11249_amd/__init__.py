@@ -93,6 +93,7 @@ _SIGS = {
     "dlmc_set_trace": (i32, [vp, TRACE_FN, vp]),
     "dlmc_forward_logits": (i32, [vp, vp, i32, i32, vp, vp, vp]),
     "dlmc_entropy_cdf": (i32, [vp, vp, i32, i32, vp, vp, vp, vp]),
+    "dlmc_entropy_cdf_noalloc": (i32, [vp, vp, i32, i32, vp, vp, vp, vp]),
     "dlmc_select": (i32, [vp, vp, vp, i32, i32, i32, f32, i32, i32, vp, vp, vp]),
     "dlmc_weight_copy": (i32, [vp, i32, vp, u64]),
     "dlmc_profile_enable": (i32, [vp, ctypes.c_uint32]),
@@ -366,6 +367,26 @@ class Model:
             g, cdf = g.view(n, V), cdf.view(n, V + 1)
         return H, mx, g, cdf
 
+
+    def entropy_cdf_noalloc(self, logits, cdf_bits: int, want_cdf: bool = True):
+        """entropy_cdf through the allocation-free entry point (the library's
+        static scratch); the outputs are torch tensors allocated here."""
+        import torch
+        n, V = logits.shape
+        dev = logits.device
+        H = torch.empty(n, dtype=torch.float32, device=dev)
+        mx = torch.empty(n, dtype=torch.float32, device=dev)
+        g = cdf = None
+        if want_cdf:
+            g = torch.empty(n * V, dtype=torch.int32, device=dev)
+            cdf = torch.empty(n * (V + 1), dtype=torch.int32, device=dev)
+        self.set_stream(torch.cuda.current_stream(dev).cuda_stream)
+        _check(lib().dlmc_entropy_cdf_noalloc(self.handle, _ptr(logits.contiguous()), n, cdf_bits,
+                                              _ptr(H), _ptr(mx), _ptr(g), _ptr(cdf)))
+        torch.cuda.current_stream(dev).synchronize()
+        if want_cdf:
+            g, cdf = g.view(n, V), cdf.view(n, V + 1)
+        return H, mx, g, cdf
 
     def context_scores(self, tokens) -> np.ndarray:
         """Attention-based context score of every position of one chunk."""

@@ -23,7 +23,7 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950",
           "-ffp-contract=off",
           "-Wno-unused-command-line-argument"]
 SOURCES = ["gemm_bf16.hip", "attention.hip", "elementwise.hip", "coding.hip", "ranking.hip", "context.hip",
-           "model.cpp", "session.cpp", "compress.cpp", "capi.cpp"]
+           "scratch.hip", "model.cpp", "session.cpp", "compress.cpp", "capi.cpp"]
 LIBS = ["-lz", "-ldl"]
 # per-source flags: attention produces no NaN from finite inputs, so max()
 # needs no NaN canonicalisation of the MFMA results (infinities keep their

@@ -273,6 +273,39 @@ dlmc_status dlmc_entropy_cdf(dlmc_model* m, const float* logits, int32_t n_rows,
   });
 }
 
+dlmc_status dlmc_entropy_cdf_noalloc(dlmc_model* m, const float* logits, int32_t n_rows,
+                                     int32_t cdf_bits, float* entropy_bits, float* row_max,
+                                     uint32_t* g, uint32_t* cdf) {
+  return guard([&] {
+    use(m);
+    DLMC_CHECK(logits && entropy_bits && row_max && n_rows >= 0, DLMC_E_INVAL, "bad argument");
+    const int V = m->cfg.vocab;
+    hipStream_t s = m->stream;
+    // the scratch holds sel_row[n] and n_sel[n], then (256-byte aligned) the
+    // CDF segment partials
+    const size_t ws_off = ((size_t)n_rows * 8 + 255) & ~(size_t)255;
+    const size_t need = cdf ? ws_off + cdf_workspace_bytes((size_t)n_rows, V) : 0;
+    if (cdf) {
+      DLMC_CHECK(cdf_bits >= 2 && cdf_bits <= 31 && (1ll << cdf_bits) > V, DLMC_E_INVAL,
+                 "cdf_bits must be in 2..31 with 2^cdf_bits > vocab");
+      DLMC_CHECK(n_rows <= 65535, DLMC_E_INVAL, "at most 65535 CDF rows per call");
+      DLMC_CHECK(need <= SCRATCH_BYTES, DLMC_E_INVAL,
+                 "n_rows needs " + std::to_string(need) + " bytes of scratch; the static scratch holds " +
+                     std::to_string(SCRATCH_BYTES));
+    }
+    DLMC_CHECK(m->scratch, DLMC_E_DEVICE, "no static scratch on this device");
+    entropy_rows(s, logits, n_rows, nullptr, V, entropy_bits, row_max);
+    if (cdf && n_rows > 0) {
+      uint8_t* base = (uint8_t*)m->scratch;
+      int32_t* sel_row = (int32_t*)base;
+      int32_t* n_sel = sel_row + n_rows;
+      void* ws = base + ws_off;
+      fill_row_slots(s, sel_row, n_sel, n_rows);
+      cdf_rows(s, logits, row_max, sel_row, n_sel, n_rows, 1, V, cdf_bits, cdf, g, ws);
+    }
+  });
+}
+
 dlmc_status dlmc_select(dlmc_model* m, const float* H, const int32_t* rows, int32_t n_rows,
                         int32_t B, int32_t T, float tau_bits, int32_t m_min, int32_t m_max,
                         int32_t* sel_pos, int32_t* sel_row, int32_t* n_sel) {

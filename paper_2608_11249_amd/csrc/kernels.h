@@ -87,6 +87,15 @@ inline size_t cdf_workspace_bytes(size_t slots, int V) {
 void cdf_rows(hipStream_t st, const float* logits, const float* mx, const int32_t* sel_row,
               const int32_t* n_sel, int B, int m_max, int V, int P, uint32_t* cdf,
               uint32_t* g_out, void* seg_ws);
+// ---------------------------------------------------------------- static scratch
+// Bytes of the static device scratch used by the allocation-free entry point.
+constexpr size_t SCRATCH_BYTES = DLMC_SCRATCH_BYTES;
+// Device address of `device`'s copy of the scratch (looked up on first use,
+// with that device current; each GPU holds its own copy).
+void* scratch_address(int device);
+// sel_row[i] = i, n_sel[i] = 1 for i < n (one committed row per "chunk")
+void fill_row_slots(hipStream_t st, int32_t* sel_row, int32_t* n_sel, int n);
+
 // test hook: a NaN into logits[0] when n_dev[0] > 0
 void poison_first_logit(hipStream_t st, float* logits, const int32_t* n_dev);
 // encode: (start, freq) of the true symbol of every committed position and reveal it

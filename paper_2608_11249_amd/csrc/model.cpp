@@ -173,6 +173,7 @@ void create_model(dlmc_model* m, const dlmc_model_config& cfg, uint64_t seed, in
   DLMC_CHECK(device >= 0 && device < ndev, DLMC_E_INVAL, "no such HIP device");
   m->device = device;
   DLMC_HIP(hipSetDevice(device));
+  m->scratch = scratch_address(device);  // looked up once per device, with it current
   DLMC_HIP(hipStreamCreateWithFlags(&m->own_stream, hipStreamNonBlocking));
   m->stream = m->own_stream;
   m->cfg = cfg;

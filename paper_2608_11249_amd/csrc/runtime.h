@@ -52,6 +52,7 @@ struct dlmc_model {
   int32_t* tokens_dev = nullptr;
   size_t tokens_cap = 0;
 
+  void* scratch = nullptr;  // this device's copy of the library's static scratch
   bool inject_nan = false;  // test hook: a NaN into the first logit of every forward
   dlmc_trace_fn trace = nullptr;
   void* trace_user = nullptr;
