@@ -283,10 +283,10 @@ dlmc_status dlmc_entropy_cdf(dlmc_model* model, const float* logits, int32_t n_r
  * which must hold 8 n_rows bytes rounded up to 256 plus
  * 20 n_rows ceil(vocab / 4096) bytes when a CDF is asked for (about 6600
  * rows at vocab 126464); larger requests fail with E_INVAL before any work.
- * Asynchronous: the results are complete when the model's stream
- * (dlmc_set_stream) reaches the end of the call's work.  Every call on a GPU
- * shares that GPU's scratch, so calls that overlap in time on one GPU (other
- * streams, other host threads, other model handles) race: serialise them. */
+ * Like dlmc_entropy_cdf it returns once its work on the model's stream is
+ * complete.  Every call on a GPU shares that GPU's scratch, so calls that
+ * overlap in time on one GPU (other host threads, other model handles)
+ * race: serialise them. */
 #define DLMC_SCRATCH_BYTES (4u << 20)
 dlmc_status dlmc_entropy_cdf_noalloc(dlmc_model* model, const float* logits, int32_t n_rows,
                                      int32_t cdf_bits, float* entropy_bits, float* row_max,

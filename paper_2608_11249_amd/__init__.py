@@ -383,7 +383,6 @@ class Model:
         self.set_stream(torch.cuda.current_stream(dev).cuda_stream)
         _check(lib().dlmc_entropy_cdf_noalloc(self.handle, _ptr(logits.contiguous()), n, cdf_bits,
                                               _ptr(H), _ptr(mx), _ptr(g), _ptr(cdf)))
-        torch.cuda.current_stream(dev).synchronize()
         if want_cdf:
             g, cdf = g.view(n, V), cdf.view(n, V + 1)
         return H, mx, g, cdf

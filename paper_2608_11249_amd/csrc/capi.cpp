@@ -303,6 +303,7 @@ dlmc_status dlmc_entropy_cdf_noalloc(dlmc_model* m, const float* logits, int32_t
       fill_row_slots(s, sel_row, n_sel, n_rows);
       cdf_rows(s, logits, row_max, sel_row, n_sel, n_rows, 1, V, cdf_bits, cdf, g, ws);
     }
+    DLMC_HIP(hipStreamSynchronize(s));
   });
 }
 
