@@ -257,8 +257,9 @@ dlmc_status dlmc_set_trace(dlmc_model* model, dlmc_trace_fn fn, void* user);
 /* ---- stage hooks (device pointers; tests and benchmarks) ---------------- */
 
 /* Test hook for the error path of non-finite model output: while `on` is
- * nonzero, every forward pass of the model writes a NaN into the first logit
- * of its first head row, so that encoding fails with E_NUMERIC. */
+ * nonzero, every forward pass of the model writes a NaN into the final-norm
+ * input of its first LM-head row, so that row's logits and entropy are
+ * non-finite and encoding fails with E_NUMERIC. */
 dlmc_status dlmc_test_inject_nonfinite(dlmc_model* model, int32_t on);
 
 /* One forward pass (Definition 3) over device state[B*T] (int32, MASK =

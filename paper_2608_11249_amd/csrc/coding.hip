@@ -8,6 +8,7 @@
 #include <climits>
 
 #include "kernels.h"
+#include "rowstats.h"
 
 namespace dlmc {
 namespace {
@@ -57,80 +58,62 @@ compact_kernel(const int32_t* __restrict__ state, int B, int T, int mask_id,
 }
 
 // ---------------------------------------------------------------- entropy
-// Online softmax statistics of a set of logits relative to its max m:
-// Z = sum e^(l-m), A = sum e^(l-m) (l-m).  H_nats = ln Z - A / Z.
-struct Stat {
-  float m, Z, A;
-};
+// Row statistics in the fixed partition of rowstats.h: the LM head's
+// epilogue writes the statistics of every 128-column group (stats_merge_kernel
+// merges them); row_stats_kernel computes the same groups from stored logits
+// and merges them in the same order, so both give the same bits.
 
-// e^t for t <= 0 on the hardware 2^x (a few ulps of fp32, far inside the
-// entropy tolerance; the kernel is bound by this arithmetic, not by memory,
-// with the accurate expf)
-__device__ __forceinline__ float exp_neg(float t) {
-  return __builtin_amdgcn_exp2f(t * 1.4426950408889634f);
-}
-
-__device__ __forceinline__ Stat merge(Stat x, Stat y) {
-  if (y.Z == 0.0f) return x;
-  if (x.Z == 0.0f) return y;
-  const float m = fmaxf(x.m, y.m);
-  const float cx = exp_neg(x.m - m), cy = exp_neg(y.m - m);
-  Stat r;
-  r.m = m;
-  r.Z = cx * x.Z + cy * y.Z;
-  r.A = cx * (x.A + (x.m - m) * x.Z) + cy * (y.A + (y.m - m) * y.Z);
-  return r;
-}
-
-__device__ __forceinline__ void add4(Stat& s, f32x4 v) {
-  const float mx = fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w));
-  if (mx > s.m) {
-    if (s.Z > 0.0f) {
-      const float c = exp_neg(s.m - mx);
-      s.A = c * (s.A + (s.m - mx) * s.Z);
-      s.Z = c * s.Z;
-    }
-    s.m = mx;
-  }
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    if (v[e] == -INFINITY) continue;  // padding of a ragged row
-    const float t = v[e] - s.m;
-    const float p = exp_neg(t);
-    s.Z += p;
-    s.A += p * t;
-  }
-}
-
+// One row per block of 256 threads.  Groups are taken 256 at a time: thread
+// t computes group 256 c + t into LDS, and lane l of wave 0 folds groups
+// 256 c + l, + 64, + 128, + 192 into its running statistic -- the fold order
+// of stats_merge_kernel.
 __global__ void __launch_bounds__(256)
-entropy_kernel(const float* __restrict__ logits, const int32_t* __restrict__ n_dev, int V,
-               float* __restrict__ H, float* __restrict__ mx) {
-  __shared__ Stat red[4];
+row_stats_kernel(const float* __restrict__ logits, const int32_t* __restrict__ n_dev, int V,
+                 float* __restrict__ H, float* __restrict__ mx) {
+  __shared__ RowStat part[256];
   const int row = blockIdx.x;
   if (n_dev && row >= *n_dev) return;
   const float* lg = logits + (size_t)row * V;
-  Stat s{-INFINITY, 0.0f, 0.0f};
-  if ((V & 3) == 0) {
-    for (int v = threadIdx.x * 4; v < V; v += 1024) add4(s, *reinterpret_cast<const f32x4*>(lg + v));
-  } else {
-    for (int v = threadIdx.x * 4; v < V; v += 1024) {
-      f32x4 x;
+  const int tid = threadIdx.x;
+  const int G = stat_groups(V);
+  const bool aligned = (V & 3) == 0;  // every group starts 16-byte aligned
+  RowStat acc{-INFINITY, 0.0f, 0.0f};
+  for (int g0 = 0; g0 < G; g0 += 256) {
+    const int g = g0 + tid;
+    if (g < G) {
+      const int c = g * STAT_GROUP;
+      part[tid] = group_stat(lg + c, min(STAT_GROUP, V - c), aligned);
+    }
+    __syncthreads();
+    if (tid < 64)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) x[e] = v + e < V ? lg[v + e] : -INFINITY;
-      add4(s, x);
+      for (int k = 0; k < 4; ++k)
+        if (g0 + tid + 64 * k < G) acc = stat_merge(acc, part[tid + 64 * k]);
+    __syncthreads();
+  }
+  if (tid < 64) {
+    acc = stat_butterfly<64>(acc);
+    if (tid == 0) {
+      H[row] = stat_entropy_bits(acc);
+      mx[row] = acc.m;
     }
   }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    Stat t{__shfl_xor(s.m, o), __shfl_xor(s.Z, o), __shfl_xor(s.A, o)};
-    s = merge(s, t);
-  }
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    Stat r = merge(merge(merge(red[0], red[1]), red[2]), red[3]);
-    H[row] = (logf(r.Z) - r.A / r.Z) * 1.4426950408889634f;
-    mx[row] = r.m;
+}
+
+// Merge of the group statistics stats[row * ld + g], g < G, one wave per row.
+__global__ void __launch_bounds__(256)
+stats_merge_kernel(const RowStat* __restrict__ stats, int ld, int G, const int32_t* __restrict__ n_dev,
+                   int n_max, float* __restrict__ H, float* __restrict__ mx) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int n = n_dev ? min(*n_dev, n_max) : n_max;
+  if (row >= n) return;
+  const RowStat* s = stats + (size_t)row * ld;
+  RowStat acc{-INFINITY, 0.0f, 0.0f};
+  for (int g = lane; g < G; g += 64) acc = stat_merge(acc, s[g]);
+  acc = stat_butterfly<64>(acc);
+  if (lane == 0) {
+    H[row] = stat_entropy_bits(acc);
+    mx[row] = acc.m;
   }
 }
 
@@ -379,9 +362,14 @@ __global__ void __launch_bounds__(256) cdf_pass_c(CdfArgs c) {
   }
 }
 
-// a quiet NaN in the first logit of the first row, if any row exists
-__global__ void poison_kernel(float* __restrict__ logits, const int32_t* __restrict__ n_dev) {
-  if (threadIdx.x == 0 && n_dev[0] > 0) logits[0] = __builtin_nanf("");
+// a quiet NaN in element 0 of the first head input row, if any row exists
+__global__ void poison_kernel(void* __restrict__ rows, int bf16, const int32_t* __restrict__ n_dev) {
+  if (threadIdx.x == 0 && n_dev[0] > 0) {
+    if (bf16)
+      *(bf16_t*)rows = 0x7FC0u;
+    else
+      *(float*)rows = __builtin_nanf("");
+  }
 }
 
 // ---------------------------------------------------------------- reveal
@@ -421,7 +409,15 @@ void compact_masked(hipStream_t st, const int32_t* state, int B, int T, int mask
 void entropy_rows(hipStream_t st, const float* logits, int n_max, const int32_t* n_dev, int V,
                   float* H, float* mx) {
   if (n_max <= 0) return;
-  entropy_kernel<<<n_max, 256, 0, st>>>(logits, n_dev, V, H, mx);
+  row_stats_kernel<<<n_max, 256, 0, st>>>(logits, n_dev, V, H, mx);
+  DLMC_HIP(hipGetLastError());
+}
+
+void entropy_merge(hipStream_t st, const void* stats, int ld, int V, int n_max, const int32_t* n_dev,
+                   float* H, float* mx) {
+  if (n_max <= 0) return;
+  stats_merge_kernel<<<ceil_div(n_max, 4), 256, 0, st>>>((const RowStat*)stats, ld, stat_groups(V),
+                                                          n_dev, n_max, H, mx);
   DLMC_HIP(hipGetLastError());
 }
 
@@ -468,8 +464,8 @@ void cdf_rows(hipStream_t st, const float* logits, const float* mx, const int32_
   DLMC_HIP(hipGetLastError());
 }
 
-void poison_first_logit(hipStream_t st, float* logits, const int32_t* n_dev) {
-  poison_kernel<<<1, 64, 0, st>>>(logits, n_dev);
+void poison_head_input(hipStream_t st, void* rows, int bf16, const int32_t* n_dev) {
+  poison_kernel<<<1, 64, 0, st>>>(rows, bf16, n_dev);
   DLMC_HIP(hipGetLastError());
 }
 

@@ -19,6 +19,7 @@
 // which other rows are in the launch, so results are identical for any batch
 // composition.
 #include "kernels.h"
+#include "rowstats.h"
 
 #include <type_traits>
 #include <utility>
@@ -93,12 +94,31 @@ __device__ __forceinline__ float rot_hi(float lo, float hi, float c, float s) {
   return fmaf(hi, c, lo * s);
 }
 
+// Softmax statistics of every 128-column group of the rows of a staged fp32
+// tile (rowstats.h): sf holds tile rows [0, R) at pitch PF, the tile's
+// first row and column are m0 and n0; one thread per (row, group), the
+// group folded in column order from LDS.
+template <int R, int BN, int PF, int NT>
+__device__ __forceinline__ void tile_group_stats(const float* sf, int m0, int n0, int tid, int Mv,
+                                                 int N, const EpiArgs& ea) {
+  constexpr int GPR = BN / STAT_GROUP;
+  static_assert(BN % STAT_GROUP == 0, "whole groups per tile");
+  for (int p = tid; p < R * GPR; p += NT) {
+    const int row = p / GPR, gi = p % GPR;
+    const int grow = m0 + row, gcol = n0 + gi * STAT_GROUP;
+    if (grow >= Mv || gcol >= N) continue;
+    const RowStat st = group_stat(sf + row * PF + gi * STAT_GROUP, min(STAT_GROUP, N - gcol), true);
+    ((RowStat*)ea.stats)[(size_t)grow * ea.stat_ld + gcol / STAT_GROUP] = st;
+  }
+}
+
 // acc[i][j][r] holds C[row][col] with row = i*32 + (r/4)*8 + lg*4 + r%4 and
 // col = j*32 + lr inside the wave tile of wave (wm, wn).
 template <int BM, int BN, int EPI, int WM, int WN>
 __device__ __forceinline__ void epilogue_w(f32x16 (&acc)[WM / 32][WN / 32], int m0, int n0, int wm,
                                            int wn, int lane, int Mv, int N, const EpiArgs& ea) {
   constexpr int TM = WM / 32, TN = WN / 32;
+  static_assert(EPI != EPI_STORE_F32, "fp32 stores go through a staged epilogue (row statistics)");
   const int lr = lane & 31, lg = lane >> 5;
   const int wrow0 = m0 + wm * WM, wcol0 = n0 + wn * WN;
   if constexpr (EPI == EPI_QKV_ROPE) {
@@ -335,6 +355,9 @@ __device__ __forceinline__ void epilogue_staged(f32x16 (&acc)[WM / 32][WN / 32],
         }
       }
     }
+    // the tile is still in LDS: the entropy's group statistics of its rows
+    if constexpr (EPI == EPI_STORE_F32)
+      if (ea.stats) tile_group_stats<BM, BN, SE::PF, NT>(sf, m0, n0, tid, Mv, N, ea);
   } else if constexpr (EPI == EPI_GELU || EPI == EPI_SWIGLU) {
     constexpr int W = EPI == EPI_GELU ? BN : BN / 2;
     constexpr int P = EPI == EPI_GELU ? SE::PB : SE::PS;
@@ -447,6 +470,9 @@ __device__ __forceinline__ void epilogue_store_halves(f32x16 (&acc)[WM / 32][WN 
         }
       }
     }
+    // the half is still in LDS: the entropy's group statistics of its rows
+    if constexpr (EPI == EPI_STORE_F32)
+      if (ea.stats) tile_group_stats<WM, BN, PF, NT>(sf, m0 + h * WM, n0, tid, Mv, N, ea);
     __syncthreads();
   }
 }
@@ -949,6 +975,7 @@ void gemm_bf16(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, i
   DLMC_CHECK((int64_t)M * K < (1ll << 31) && (int64_t)N * K < (1ll << 31), DLMC_E_INVAL,
              "GEMM operand too large for 32-bit offsets");
   if (M <= 0 || N <= 0) return;
+  DLMC_CHECK(!ea.stats || epi == EPI_STORE_F32, DLMC_E_INVAL, "row statistics need the fp32 store");
   const bool paired = (epi == EPI_QKV_ROPE || epi == EPI_SWIGLU);
   DLMC_CHECK(!paired || N % 128 == 0, DLMC_E_INVAL, "paired epilogue needs N % 128 == 0");
   DLMC_CHECK(epi != EPI_QKV_ROPE || (ea.d % 128 == 0 && (ea.dh == 64 || ea.dh == 128)),

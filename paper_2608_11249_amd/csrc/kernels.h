@@ -25,6 +25,10 @@ struct EpiArgs {
   const float* rope_cos = nullptr;  // [T, dh/2]
   const float* rope_sin = nullptr;
   int T = 0, Tp = 0, H = 0, dh = 0, d = 0;
+  // EPI_STORE_F32 (optional): softmax statistics of every 128-column group of
+  // every stored row, RowStat [rows, stat_ld] (rowstats.h)
+  void* stats = nullptr;
+  int stat_ld = 0;
 };
 
 // M_dev (optional): device int holding the live row count (<= M); rows at or
@@ -72,6 +76,10 @@ void compact_masked(hipStream_t st, const int32_t* state, int B, int T, int mask
 // per row of logits[n, V]: entropy in bits and row max (n from n_dev when given)
 void entropy_rows(hipStream_t st, const float* logits, int n_max, const int32_t* n_dev, int V,
                   float* H, float* mx);
+// the same from the 128-column group statistics the LM head's epilogue
+// wrote (stats: RowStat [n, ld]); bit-identical to entropy_rows
+void entropy_merge(hipStream_t st, const void* stats, int ld, int V, int n_max, const int32_t* n_dev,
+                   float* H, float* mx);
 // commitment schedule, one workgroup per chunk
 void select_positions(hipStream_t st, const float* H, const int32_t* rows,
                       const int32_t* chunk_off, const int32_t* chunk_cnt, int B, int T,
@@ -96,8 +104,9 @@ void* scratch_address(int device);
 // sel_row[i] = i, n_sel[i] = 1 for i < n (one committed row per "chunk")
 void fill_row_slots(hipStream_t st, int32_t* sel_row, int32_t* n_sel, int n);
 
-// test hook: a NaN into logits[0] when n_dev[0] > 0
-void poison_first_logit(hipStream_t st, float* logits, const int32_t* n_dev);
+// test hook: a NaN into element 0 of the head's input rows (bf16 or fp32)
+// when n_dev[0] > 0, which makes the first head row non-finite
+void poison_head_input(hipStream_t st, void* rows, int bf16, const int32_t* n_dev);
 // encode: (start, freq) of the true symbol of every committed position and reveal it
 void gather_reveal(hipStream_t st, const uint32_t* cdf, const int32_t* sel_pos,
                    const int32_t* n_sel, const int32_t* tokens, const int64_t* slot_base,

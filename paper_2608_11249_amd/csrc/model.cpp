@@ -3,6 +3,7 @@
 #include <cmath>
 #include <cstring>
 
+#include "rowstats.h"
 #include "runtime.h"
 
 using namespace dlmc;
@@ -219,6 +220,7 @@ void create_model(dlmc_model* m, const dlmc_model_config& cfg, uint64_t seed, in
   if (!m->bf16) m->tmp = (float*)m->dalloc(R * std::max(3 * d, nF) * 4);
   m->hm = m->dalloc(R * d * m->esz);
   m->logits = (float*)m->dalloc(R * V * 4);
+  if (m->bf16) m->stats = m->dalloc(R * (size_t)stat_groups(V) * sizeof(RowStat));
   m->H = (float*)m->dalloc(R * 4);
   m->mx = (float*)m->dalloc(R * 4);
   m->rows = (int32_t*)m->dalloc(R * 4);
@@ -425,16 +427,25 @@ void dlmc_model::forward(const int32_t* st_dev, int B, int T, float* logits_out,
     StageTimer t(this, DLMC_STAGE_NORM, head_rows * dd * (4.0 + es));
     norm_rows(s, x, hm, cfg.dtype, M, d, cfg.norm_kind, cfg.norm_eps, rw, nr);
   }
+  if (inject_nan) poison_head_input(s, hm, bf16 ? 1 : 0, nr);
   EpiArgs o;
   o.out = lg;
   o.ldo = V;
+  o.stats = stats;  // the entropy's group statistics, fused into the head's epilogue
+  o.stat_ld = stat_groups(V);
   StageTimer t(this, DLMC_STAGE_HEAD, 2.0 * head_rows * V * dd);
   if (bf16)
     gemm_bf16(s, (const bf16_t*)hm, (const bf16_t*)this->head, M, V, d, nr, EPI_STORE_F32, o,
               rows_hint >= 0 ? (int)rows_hint : -1);
   else
     gemm_f32(s, (const float*)hm, (const float*)this->head, M, V, d, nr, EPI_STORE_F32, o);
-  if (inject_nan) poison_first_logit(s, lg, nr);
+}
+
+void dlmc_model::row_stats(int n_max) {
+  if (bf16)
+    entropy_merge(stream, stats, stat_groups(cfg.vocab), cfg.vocab, n_max, n_rows, H, mx);
+  else
+    entropy_rows(stream, logits, n_max, n_rows, cfg.vocab, H, mx);
 }
 
 void dlmc_model::context_scores(const int32_t* tokens, int T, std::vector<float>& score) {

@@ -39,6 +39,7 @@ struct dlmc_model {
   float* tmp = nullptr;  // fp32 model only: [rows, max(3d, 2F)]
   void* hm = nullptr;    // final-norm rows of masked positions [rows, d]
   float* logits = nullptr;  // [rows, V]
+  void* stats = nullptr;    // bf16 head: softmax statistics per 128-column group [rows, G]
   float *H = nullptr, *mx = nullptr;
   int32_t *rows = nullptr, *n_rows = nullptr, *chunk_off = nullptr, *chunk_cnt = nullptr;
   int32_t *state = nullptr, *err = nullptr;
@@ -96,6 +97,10 @@ struct dlmc_model {
   int32_t* ctx_state = nullptr;
   int ctx_T = 0;
   void context_scores(const int32_t* tokens, int T, std::vector<float>& score);
+  // entropy (bits) and max of the first n_rows[0] (at most n_max) head rows of
+  // the last forward into H / mx: merged from the head's group statistics
+  // (bf16), or from the stored logits (fp32); both give the same bits
+  void row_stats(int n_max);
 };
 
 namespace dlmc {

@@ -12,6 +12,7 @@
 #include <cmath>
 #include <cstring>
 
+#include "rowstats.h"
 #include "runtime.h"
 
 using namespace dlmc;
@@ -299,8 +300,9 @@ int dlmc_session::step(uint64_t* coded) {
   if (cp.schedule == DLMC_SCHED_ENTROPY) {
     m->forward(m->state, B, T, nullptr, nullptr, nullptr, masked);
     {
-      StageTimer t(m, DLMC_STAGE_ENTROPY, (double)masked * V * 4.0);
-      entropy_rows(s, m->logits, B * T, m->n_rows, V, m->H, m->mx);
+      StageTimer t(m, DLMC_STAGE_ENTROPY, m->bf16 ? (double)masked * stat_groups(V) * sizeof(RowStat)
+                                                  : (double)masked * V * 4.0);
+      m->row_stats(B * T);
     }
     {
       StageTimer t(m, DLMC_STAGE_SELECT, (double)masked * 8.0);
@@ -331,8 +333,9 @@ int dlmc_session::step(uint64_t* coded) {
     m->forward(m->state, B, T, nullptr, nullptr, nullptr, r, true);
     {
       // row statistics (the maximum feeds the CDF) at the committed rows only
-      StageTimer t(m, DLMC_STAGE_ENTROPY, (double)r * V * 4.0);
-      entropy_rows(s, m->logits, B * T, m->n_rows, V, m->H, m->mx);
+      StageTimer t(m, DLMC_STAGE_ENTROPY, m->bf16 ? (double)r * stat_groups(V) * sizeof(RowStat)
+                                                  : (double)r * V * 4.0);
+      m->row_stats(B * T);
     }
   }
   const bool rank = cp.coder == DLMC_CODER_RANK;

@@ -531,3 +531,40 @@ def test_encode_range_and_merge_byte_identical(kw):
         with pytest.raises(dl.DlmcError) as e:
             m1.encode_range(toks, cd, 5, 2)
         assert e.value.code == -1
+
+
+@pytest.mark.parametrize("kw,T,V", [
+    (dict(ffn="swiglu", norm="rmsnorm"), 96, 500),       # 128 x 128 head tiles, ragged group
+    (dict(d_model=512, n_heads=4, d_ffn=1024), 300, 384),  # 256 x 128 head tiles
+    (dict(d_model=128, n_heads=1, d_ffn=256), 600, 98304),  # 256 x 256 head tiles
+])
+def test_fused_head_statistics_equal_standalone(kw, T, V):
+    """The entropies the encoder uses come from softmax statistics fused into
+    the LM head's epilogue; at every pass they must equal, bit for bit, the
+    standalone statistics kernel on the stored logits of the same state (one
+    128-column partition for both, whatever the head's tile shape)."""
+    sh = shape(vocab=V, **kw)
+    k = T // 8
+    cd = codec(T, k=k, P=24, W=64)
+    toks = wl.markov1_tokens(T, V, 8)
+    log("fused head statistics", kw, T, V)
+    recs = {}
+
+    def tr(d, chunk, pas, pos, ent, h):
+        if d == 0:
+            recs[pas] = (pos, ent)
+
+    with dl.Model(sh, max_chunk=T) as m:
+        m.set_trace(tr)
+        m.encode(toks, cd)
+        m.set_trace(None)
+        state = np.full(T, sh.mask_id, dtype=np.int64)
+        for p in sorted(recs):
+            pos, ent = recs[p]
+            lg, rows = m.forward_logits(dev_state(state[None, :]))
+            H, mx, _, _ = m.entropy_cdf(lg, 24, want_cdf=False)
+            H, rows = H.cpu().numpy(), rows.cpu().numpy()
+            row_of = {int(r): i for i, r in enumerate(rows)}
+            got = np.array([H[row_of[q]] for q in pos], dtype=np.float32)
+            assert np.array_equal(got, np.array(ent, dtype=np.float32)), p
+            state[pos] = toks[pos]
