@@ -19,6 +19,12 @@
 // chunks.  A block holds QB = 128 or 256 queries (4 or 8 waves, two waves per
 // SIMD either way); with 256 every K / V tile moved into LDS serves twice as
 // many queries, which halves the tile traffic per CU.
+//
+// Tiles go through a ring of NB LDS buffers, issued NB - 1 tiles ahead.  The
+// end of a tile waits (s_waitcnt vmcnt) only for the loads of the next tile
+// -- those of the tiles after it stay in flight -- and then meets the other
+// waves at a bare s_barrier: __syncthreads() would also wait for every direct
+// load still in flight, which would take away the lookahead.
 #include <type_traits>
 
 #include "kernels.h"
@@ -53,7 +59,20 @@ __device__ __forceinline__ void lds_dma16(const bf16_t* g, bf16_t* lds) {
 #endif
 }
 
-template <int DH, int QB>
+// s_barrier without the memory fence of __syncthreads(), which would also wait
+// for the direct loads still in flight
+__device__ __forceinline__ void block_barrier() {
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// s_waitcnt immediate: vmcnt(n) with lgkmcnt(0)
+constexpr int waitcnt_vm(int n) { return 0x0070 | (n & 15) | ((n >> 4) << 14); }
+
+template <int DH, int QB, int NB>
 __global__ void __launch_bounds__(2 * QB, 256 / QB)
 attn_bf16_kernel(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kg,
                  const bf16_t* __restrict__ Vt, bf16_t* __restrict__ O, int H, int T, int Tp,
@@ -66,8 +85,10 @@ attn_bf16_kernel(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kg,
   constexpr int VW = DH / 8 / NWV;   // V^T windows (8 rows of 128 B) per wave
   static_assert(KW >= 1 && VW >= 1 && KW * KRW * NWV == KT && VW * 8 * NWV == DH, "tile split");
   constexpr int NV = DH / 32 * 4;    // PV MFMAs per tile
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[2][KT * DH];
-  __shared__ __attribute__((aligned(16))) bf16_t Vs[2][DH * KT];
+  constexpr int NL = KW + VW;        // direct loads per wave per tile
+  static_assert(NB >= 2 && (NB - 2) * NL < 64, "ring size / vmcnt field");
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[NB][KT * DH];
+  __shared__ __attribute__((aligned(16))) bf16_t Vs[NB][DH * KT];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 31, lg = lane >> 5;
@@ -148,9 +169,11 @@ attn_bf16_kernel(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kg,
   const char* ks_base = reinterpret_cast<const char*>(&Ks[0][0]);
   const char* vs_base = reinterpret_cast<const char*>(&Vs[0][0]);
   auto tile = [&](int kt, auto cur_c) {
-    constexpr int cur = decltype(cur_c)::value;
+    constexpr int cur = decltype(cur_c)::value;  // kt % NB
     const int k0 = kt * KT;
-    if (kt + 1 < n_kt) load_tile(kt + 1, cur ^ 1);
+    // tile kt + NB - 1 goes into the buffer of tile kt - 1, which every wave
+    // finished reading before the barrier that ended tile kt - 1
+    if (kt + NB - 1 < n_kt) load_tile(kt + NB - 1, (cur + NB - 1) % NB);
 
     // S^T for LDS rows 0-31 (s0) and 32-63 (s1); fragments two k steps ahead
     f32x16 s0, s1;
@@ -233,18 +256,31 @@ attn_bf16_kernel(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kg,
       if (idx + 2 < NV) vload(idx + 2, vf[(idx + 2) % 3]);
       o[idx >> 2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[idx % 3], pf[idx & 3], o[idx >> 2], 0, 0, 0);
     }
-    // the next tile has landed (own loads) and every wave is done with this one
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
+    // tile kt + 1 has landed (this wave's loads; the NB - 2 tiles after it
+    // may still be in flight), and after the barrier every wave's have, and
+    // every wave is done with tile kt
+    if (kt + NB - 1 < n_kt)
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm((NB - 2) * NL));
+    else
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+    block_barrier();
   };
 
-  load_tile(0, 0);
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-  // two tiles per trip, so each trip's buffer offsets are constants
-  for (int kt = 0; kt < n_kt; kt += 2) {
+  // prologue: tiles 0 .. NB - 2; tile 0 landed before the loop
+#pragma unroll
+  for (int t = 0; t < NB - 1; ++t)
+    if (t < n_kt) load_tile(t, t);
+  if (NB - 1 <= n_kt)
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm((NB - 2) * NL));
+  else
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+  block_barrier();
+  // NB tiles per trip, so each trip's buffer offsets are constants
+  for (int kt = 0; kt < n_kt; kt += NB) {
     tile(kt, std::integral_constant<int, 0>{});
     if (kt + 1 < n_kt) tile(kt + 1, std::integral_constant<int, 1>{});
+    if constexpr (NB >= 3)
+      if (kt + 2 < n_kt) tile(kt + 2, std::integral_constant<int, 2 % NB>{});
   }
 
   const int q = q0 + lr;
@@ -332,8 +368,11 @@ void attention_bf16(hipStream_t st, const bf16_t* q, const bf16_t* k, const bf16
   const bool wide = Tp % 256 == 0 && (long)(Tp / 256) * H * B >= 256;
   auto run = [&](auto dh_c, auto qb_c) {
     constexpr int DH = decltype(dh_c)::value, QB = decltype(qb_c)::value;
+    // three tile buffers (96 KB) for one 256-query block per CU; two (64 KB)
+    // keep two 128-query blocks per CU
+    constexpr int NB = QB == 256 ? 3 : 2;
     dim3 grid(ceil_div(T, QB) * H * B), block(2 * QB);
-    attn_bf16_kernel<DH, QB><<<grid, block, 0, st>>>(q, k, vt, out, H, T, Tp, scale_log2);
+    attn_bf16_kernel<DH, QB, NB><<<grid, block, 0, st>>>(q, k, vt, out, H, T, Tp, scale_log2);
   };
   using I64 = std::integral_constant<int, 64>;
   using I128 = std::integral_constant<int, 128>;
