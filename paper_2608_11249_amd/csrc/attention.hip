@@ -86,7 +86,8 @@ attn_bf16_kernel(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kg,
   static_assert(KW >= 1 && VW >= 1 && KW * KRW * NWV == KT && VW * 8 * NWV == DH, "tile split");
   constexpr int NV = DH / 32 * 4;    // PV MFMAs per tile
   constexpr int NL = KW + VW;        // direct loads per wave per tile
-  static_assert(NB >= 2 && (NB - 2) * NL < 64, "ring size / vmcnt field");
+  constexpr int LA = NB - 1;         // tiles loaded ahead
+  static_assert(LA >= 1 && (LA - 1) * NL < 64 && NB <= 3, "ring size / vmcnt field");
   __shared__ __attribute__((aligned(16))) bf16_t Ks[NB][KT * DH];
   __shared__ __attribute__((aligned(16))) bf16_t Vs[NB][DH * KT];
 
@@ -168,34 +169,41 @@ attn_bf16_kernel(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kg,
   const int n_kt = (T + KT - 1) / KT;
   const char* ks_base = reinterpret_cast<const char*>(&Ks[0][0]);
   const char* vs_base = reinterpret_cast<const char*>(&Vs[0][0]);
-  auto tile = [&](int kt, auto cur_c) {
-    constexpr int cur = decltype(cur_c)::value;  // kt % NB
-    const int k0 = kt * KT;
-    // tile kt + NB - 1 goes into the buffer of tile kt - 1, which every wave
-    // finished reading before the barrier that ended tile kt - 1
-    if (kt + NB - 1 < n_kt) load_tile(kt + NB - 1, (cur + NB - 1) % NB);
-
-    // S^T for LDS rows 0-31 (s0) and 32-63 (s1); fragments two k steps ahead
-    f32x16 s0, s1;
+  // S^T of the tile in buffer `cur` for LDS rows 0-31 (s0) and 32-63 (s1).
+  // Fragment reads run KA k steps ahead of the MFMAs; the scheduling fences
+  // keep the compiler from sinking them next to their use, which would expose
+  // the LDS latency at every step.  The last steps also start the reads of
+  // the first VA V^T fragments of the same tile, for the PV product.
+  constexpr int KA = NS < 4 ? NS : 4;
+  constexpr int VA = 4;
+  auto scores = [&](int cur, f32x16& s0, f32x16& s1, bf16x8(&vf)[VA]) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) s0[r] = s1[r] = 0.0f;
     const char* kb = ks_base + cur * KT * DH * 2;
-    bf16x8 kf[3][2];
+    const char* vb = vs_base + cur * DH * KT * 2;
+    bf16x8 kf[KA][2];
     auto kload = [&](int s, bf16x8(&f)[2]) {
       f[0] = *reinterpret_cast<const bf16x8*>(kb + koff[s][0]);
       f[1] = *reinterpret_cast<const bf16x8*>(kb + koff[s][1]);
     };
-    kload(0, kf[0]);
-    kload(1, kf[1]);
+#pragma unroll
+    for (int s = 0; s < KA; ++s) kload(s, kf[s]);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      if (s + 2 < NS) kload(s + 2, kf[(s + 2) % 3]);
-      s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s % 3][0], qf[s], s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s % 3][1], qf[s], s1, 0, 0, 0);
+      s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s % KA][0], qf[s], s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s % KA][1], qf[s], s1, 0, 0, 0);
+      if (s + KA < NS) kload(s + KA, kf[s % KA]);
+      if (s + KA >= NS && s + KA - NS < VA)
+        vf[s + KA - NS] = *reinterpret_cast<const bf16x8*>(vb + voff[s + KA - NS]);
+      __builtin_amdgcn_sched_barrier(0);
     }
+  };
 
-    // online softmax (base 2) for query q0 + lr.  Register r of s0 holds key
-    // 16 (r >> 3) + 8 lg + (r & 7) of the tile (s1: + 32).
+  // online softmax (base 2) of the tile starting at key k0 for query q0 + lr,
+  // leaving the P^T fragments in pf.  Register r of s0 holds key
+  // 16 (r >> 3) + 8 lg + (r & 7) of the tile (s1: + 32).
+  auto softmax = [&](int k0, f32x16& s0, f32x16& s1, bf16x8(&pf)[4]) {
     if (k0 + KT > T) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
@@ -234,10 +242,8 @@ attn_bf16_kernel(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kg,
     float psum = (ps[0] + ps[1]) + (ps[2] + ps[3]);
     psum += __shfl_xor(psum, 32);
     l_run += psum;
-
     // P^T fragment of k step j: keys 16 j + 8 lg .. + 7 = registers
     // 8 (j % 2) .. + 7 of tile j / 2
-    bf16x8 pf[4];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       pf[0][e] = (__bf16)s0[e];
@@ -245,33 +251,51 @@ attn_bf16_kernel(const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kg,
       pf[2][e] = (__bf16)s1[e];
       pf[3][e] = (__bf16)s1[8 + e];
     }
-    // O^T += V^T P^T; the V^T fragment of row d, k step j is chunk 2 j + lg
+  };
+
+  // O^T += V^T P^T with the V^T tile in buffer `cur`; the V^T fragment of
+  // row d, k step j is chunk 2 j + lg.  Reads run VA MFMAs ahead; the first
+  // VA are already in vf (started by the scores of the same tile).
+  auto pv = [&](int cur, const bf16x8(&pf)[4], bf16x8(&vf)[VA]) {
     const char* vb = vs_base + cur * DH * KT * 2;
-    bf16x8 vf[3];
     auto vload = [&](int idx, bf16x8& f) { f = *reinterpret_cast<const bf16x8*>(vb + voff[idx]); };
-    vload(0, vf[0]);
-    vload(1, vf[1]);
 #pragma unroll
     for (int idx = 0; idx < NV; ++idx) {
-      if (idx + 2 < NV) vload(idx + 2, vf[(idx + 2) % 3]);
-      o[idx >> 2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[idx % 3], pf[idx & 3], o[idx >> 2], 0, 0, 0);
+      o[idx >> 2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[idx % VA], pf[idx & 3], o[idx >> 2], 0, 0, 0);
+      if (idx + VA < NV) vload(idx + VA, vf[idx % VA]);
+      __builtin_amdgcn_sched_barrier(0);
     }
-    // tile kt + 1 has landed (this wave's loads; the NB - 2 tiles after it
-    // may still be in flight), and after the barrier every wave's have, and
-    // every wave is done with tile kt
-    if (kt + NB - 1 < n_kt)
-      __builtin_amdgcn_s_waitcnt(waitcnt_vm((NB - 2) * NL));
+  };
+
+  // Interval kt: start the loads of tile kt + LA into the buffer of tile
+  // kt - 1, which every wave finished before the barrier that ended the
+  // previous interval; compute; wait until tile kt + 1 has landed (this wave's
+  // loads; the LA - 1 tiles after it may still be in flight) and meet the
+  // other waves, after which every wave's loads of tile kt + 1 have landed.
+  auto interval_end = [&](int kt) {
+    if (kt + LA < n_kt)
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm((LA - 1) * NL));
     else
       __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
     block_barrier();
   };
+  auto tile = [&](int kt, auto cur_c) {
+    constexpr int cur = decltype(cur_c)::value;  // kt % NB
+    if (kt + LA < n_kt) load_tile(kt + LA, (cur + LA) % NB);
+    f32x16 s0, s1;
+    bf16x8 vf[VA], pf[4];
+    scores(cur, s0, s1, vf);
+    softmax(kt * KT, s0, s1, pf);
+    pv(cur, pf, vf);
+    interval_end(kt);
+  };
 
-  // prologue: tiles 0 .. NB - 2; tile 0 landed before the loop
+  // prologue: tiles 0 .. LA - 1; tile 0 landed before the first interval
 #pragma unroll
-  for (int t = 0; t < NB - 1; ++t)
+  for (int t = 0; t < LA; ++t)
     if (t < n_kt) load_tile(t, t);
-  if (NB - 1 <= n_kt)
-    __builtin_amdgcn_s_waitcnt(waitcnt_vm((NB - 2) * NL));
+  if (LA <= n_kt)
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm((LA - 1) * NL));
   else
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
   block_barrier();
