@@ -262,6 +262,15 @@ dlmc_status dlmc_set_trace(dlmc_model* model, dlmc_trace_fn fn, void* user);
  * non-finite and encoding fails with E_NUMERIC. */
 dlmc_status dlmc_test_inject_nonfinite(dlmc_model* model, int32_t on);
 
+/* Test hook for the deferred LM-head logits of the entropy schedule (bf16
+ * models).  With many masked rows, the head writes only each row's entropy
+ * statistics (Schedules, item 3) and the logits of the rows committed in the
+ * pass are computed after the selection, which gives the same bits as storing
+ * them all.  mode 0 (default): decided per pass by estimated cost; 1: always
+ * deferred; 2: never.  Payloads do not depend on the mode.  E_INVAL for
+ * another mode. */
+dlmc_status dlmc_test_head_logits(dlmc_model* model, int32_t mode);
+
 /* One forward pass (Definition 3) over device state[B*T] (int32, MASK =
  * vocab).  Writes the fp32 logits at the masked positions, in ascending
  * (chunk, position) order, to logits[n_rows * vocab], their flat indices

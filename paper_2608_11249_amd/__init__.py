@@ -110,6 +110,7 @@ _SIGS = {
     "dlmc_merge": (i32, [P(vp), P(u64), i32, vp, u64, P(u64)]),
     "dlmc_numerics_id": (i32, [P(u64)]),
     "dlmc_test_inject_nonfinite": (i32, [vp, i32]),
+    "dlmc_test_head_logits": (i32, [vp, i32]),
     "dlmc_status_string": (ctypes.c_char_p, [i32]),
     "dlmc_last_error": (ctypes.c_char_p, []),
 }
@@ -270,6 +271,10 @@ class Model:
     def inject_nonfinite(self, on: bool):
         """Test hook: every forward writes a NaN into its first logit while on."""
         _check(lib().dlmc_test_inject_nonfinite(self.handle, 1 if on else 0))
+
+    def head_logits_mode(self, mode: int):
+        """Test hook: 0 deferred logits chosen by cost, 1 always, 2 never."""
+        _check(lib().dlmc_test_head_logits(self.handle, int(mode)))
 
     def decode(self, data: bytes, batch: int = 0) -> np.ndarray:
         buf = np.frombuffer(data, dtype=np.uint8).copy()

@@ -233,6 +233,14 @@ dlmc_status dlmc_test_inject_nonfinite(dlmc_model* m, int32_t on) {
   });
 }
 
+dlmc_status dlmc_test_head_logits(dlmc_model* m, int32_t mode) {
+  return guard([&] {
+    DLMC_CHECK(m, DLMC_E_INVAL, "model is NULL");
+    DLMC_CHECK(mode >= 0 && mode <= 2, DLMC_E_INVAL, "mode must be 0, 1 or 2");
+    m->head_mode = mode;
+  });
+}
+
 dlmc_status dlmc_forward_logits(dlmc_model* m, const int32_t* state, int32_t B, int32_t T,
                                 float* logits, int32_t* rows, int32_t* n_rows) {
   return guard([&] {

@@ -302,6 +302,81 @@ void init_weights(hipStream_t st, void* dst, int dtype, uint64_t seed, int tenso
   DLMC_HIP(hipGetLastError());
 }
 
+// One row per wave (d == 256 PER4): lane l holds columns 4 (l + 64 e) .. + 3
+// as 16-byte loads; the row sums are fixed-order butterflies over the wave
+// (every lane ends with the same bits), so no block barrier is needed.
+template <int PER4>
+__global__ void __launch_bounds__(256)
+norm_wave_kernel(const float* __restrict__ x, void* __restrict__ out, int out_dtype, int n_rows,
+                 int norm_kind, float eps, const int32_t* __restrict__ gather,
+                 const int32_t* __restrict__ n_dev) {
+  constexpr int d = 256 * PER4;
+  const int lane = threadIdx.x & 63;
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (i >= n_rows || (n_dev && i >= *n_dev)) return;
+  const int src = gather ? gather[i] : i;
+  const float4* xr = reinterpret_cast<const float4*>(x + (size_t)src * d);
+  float4 v[PER4];
+#pragma unroll
+  for (int e = 0; e < PER4; ++e) v[e] = xr[lane + 64 * e];
+  auto wave_sum = [](float t) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) t += __shfl_xor(t, o);
+    return t;
+  };
+  float scale, shift = 0.0f;
+  if (norm_kind == DLMC_NORM_LAYER) {
+    float s = 0.0f;
+#pragma unroll
+    for (int e = 0; e < PER4; ++e) s += (v[e].x + v[e].y) + (v[e].z + v[e].w);
+    const float mean = wave_sum(s) / (float)d;
+    float q = 0.0f;
+#pragma unroll
+    for (int e = 0; e < PER4; ++e) {
+      const float a = v[e].x - mean, b = v[e].y - mean, c = v[e].z - mean, w = v[e].w - mean;
+      q += (a * a + b * b) + (c * c + w * w);
+    }
+    const float var = wave_sum(q) / (float)d;
+    scale = 1.0f / sqrtf(var + eps);
+    shift = mean;
+  } else {
+    float s = 0.0f;
+#pragma unroll
+    for (int e = 0; e < PER4; ++e)
+      s += (v[e].x * v[e].x + v[e].y * v[e].y) + (v[e].z * v[e].z + v[e].w * v[e].w);
+    const float ms = wave_sum(s) / (float)d;
+    scale = 1.0f / sqrtf(ms + eps);
+  }
+#pragma unroll
+  for (int e = 0; e < PER4; ++e) {
+    const int c4 = lane + 64 * e;
+    const float y0 = (v[e].x - shift) * scale, y1 = (v[e].y - shift) * scale;
+    const float y2 = (v[e].z - shift) * scale, y3 = (v[e].w - shift) * scale;
+    if (out_dtype == DLMC_DTYPE_BF16) {
+      u32x2 w;
+      w[0] = (uint32_t)f32_to_bf16(y0) | ((uint32_t)f32_to_bf16(y1) << 16);
+      w[1] = (uint32_t)f32_to_bf16(y2) | ((uint32_t)f32_to_bf16(y3) << 16);
+      reinterpret_cast<u32x2*>((bf16_t*)out + (size_t)i * d)[c4] = w;
+    } else {
+      reinterpret_cast<float4*>((float*)out + (size_t)i * d)[c4] = make_float4(y0, y1, y2, y3);
+    }
+  }
+}
+
+// one block per selection slot: 16-byte chunks of the source row, or zeros
+// for a slot past its chunk's committed count
+__global__ void __launch_bounds__(256)
+gather_slot_rows_kernel(const bf16_t* __restrict__ src, const float* __restrict__ mx,
+                        const int32_t* __restrict__ sel_row, const int32_t* __restrict__ n_sel,
+                        int m_max, int d, bf16_t* __restrict__ dst, float* __restrict__ dst_mx) {
+  const int slot = blockIdx.x, b = slot / m_max, j = slot % m_max;
+  const bool live = j < n_sel[b];
+  if (threadIdx.x == 0) dst_mx[slot] = live ? mx[sel_row[slot]] : 0.0f;
+  const u32x4* s = reinterpret_cast<const u32x4*>(src + (live ? (size_t)sel_row[slot] * d : 0));
+  u32x4* o = reinterpret_cast<u32x4*>(dst + (size_t)slot * d);
+  for (int c = threadIdx.x; c < d / 8; c += blockDim.x) o[c] = live ? s[c] : u32x4{0u, 0u, 0u, 0u};
+}
+
 void embed(hipStream_t st, const int32_t* state, const void* table, int dtype, float* x,
            int n_rows, int d, int max_id) {
   if (n_rows <= 0) return;
@@ -314,6 +389,25 @@ void norm_rows(hipStream_t st, const float* x, void* out, int out_dtype, int n_r
   if (n_rows <= 0) return;
   const int per = ceil_div(d, 256);
   dim3 grid(n_rows), block(256);
+  if (d % 256 == 0 && d <= 2048) {
+    const dim3 wgrid(ceil_div(n_rows, 4));
+#define DLMC_NORMW(P)                                                                   \
+  norm_wave_kernel<P><<<wgrid, block, 0, st>>>(x, out, out_dtype, n_rows, norm_kind, eps, \
+                                               gather_rows, n_dev)
+    switch (d / 256) {
+      case 1: DLMC_NORMW(1); break;
+      case 2: DLMC_NORMW(2); break;
+      case 3: DLMC_NORMW(3); break;
+      case 4: DLMC_NORMW(4); break;
+      case 5: DLMC_NORMW(5); break;
+      case 6: DLMC_NORMW(6); break;
+      case 7: DLMC_NORMW(7); break;
+      default: DLMC_NORMW(8); break;
+    }
+#undef DLMC_NORMW
+    DLMC_HIP(hipGetLastError());
+    return;
+  }
   if (d % 1024 == 0 && d <= 8192) {
 #define DLMC_NORM4(P)                                                                           \
   norm4_kernel<P><<<grid, block, 0, st>>>(x, out, out_dtype, d, norm_kind, eps, gather_rows, \
@@ -343,6 +437,14 @@ void norm_rows(hipStream_t st, const float* x, void* out, int out_dtype, int n_r
   else if (per <= 32) DLMC_NORM(32);
   else throw Error(DLMC_E_INVAL, "d_model above 8192 is not supported");
 #undef DLMC_NORM
+  DLMC_HIP(hipGetLastError());
+}
+
+void gather_slot_rows(hipStream_t st, const bf16_t* src, const float* mx, const int32_t* sel_row,
+                      const int32_t* n_sel, int B, int m_max, int d, bf16_t* dst, float* dst_mx) {
+  DLMC_CHECK(d % 8 == 0, DLMC_E_INVAL, "row gather needs d % 8 == 0");
+  if (B <= 0 || m_max <= 0) return;
+  gather_slot_rows_kernel<<<B * m_max, 256, 0, st>>>(src, mx, sel_row, n_sel, m_max, d, dst, dst_mx);
   DLMC_HIP(hipGetLastError());
 }
 

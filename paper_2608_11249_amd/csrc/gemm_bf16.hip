@@ -332,10 +332,12 @@ __device__ __forceinline__ void epilogue_staged(f32x16 (&acc)[WM / 32][WN / 32],
     }
   }
   __syncthreads();
-  // phase 2: 16-byte chunks, a fixed number per thread
+  // phase 2: 16-byte chunks, a fixed number per thread (EPI_STORE_F32 with
+  // no output: the row statistics only)
   if constexpr (EPI == EPI_STORE_F32 || EPI == EPI_RESIDUAL) {
 #pragma unroll
     for (int it = 0; it < IT4; ++it) {
+      if (EPI == EPI_STORE_F32 && !ea.out) break;
       const int qi = tid + it * NT, row = qi / CPR4, c = (qi % CPR4) * 4;
       const int grow = m0 + row, gcol = n0 + c;
       if (grow >= Mv) continue;
@@ -451,6 +453,7 @@ __device__ __forceinline__ void epilogue_store_halves(f32x16 (&acc)[WM / 32][WN 
     __syncthreads();
 #pragma unroll
     for (int it = 0; it < IT4; ++it) {
+      if (EPI == EPI_STORE_F32 && !ea.out) break;  // row statistics only
       const int qi = tid + it * NT, row = qi / CPR4, c = (qi % CPR4) * 4;
       const int grow = m0 + h * WM + row, gcol = n0 + c;
       if (grow >= Mv) continue;
@@ -981,29 +984,37 @@ void gemm_bf16(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, i
   DLMC_CHECK(epi != EPI_QKV_ROPE || (ea.d % 128 == 0 && (ea.dh == 64 || ea.dh == 128)),
              DLMC_E_INVAL, "QKV epilogue needs d % 128 == 0 and head dim 64 or 128");
   // Tile choice (never changes the result).  Estimated time of an option:
-  // its flops over (kernel rate x share of computed rows that are live x
-  // share of the tile slots of its last wave of tiles that are filled), with
-  // the rates measured at M = 2048 with the weights streamed from HBM, as in
-  // a layer loop: 256 x 256 1.23, 256 x 128 1.10, 128 x 128 0.92 PFLOP/s.
-  // The 4-wave kernel may also split the columns: 256 x 256 tiles on the
-  // first c1, 256 x 128 tiles on the rest (one launch), so that each part
-  // fills whole waves of tiles (QKV at M = 2048: Q and K on 256 tiles, V on
-  // 256 more, instead of three waves of 256 x 128 tiles).
+  // waves of tiles x (c0 + k-tiles x c1), where c1 is a tile's main-loop time
+  // per 64-wide k-tile with every CU busy, and c0 its fixed cost (prologue
+  // and epilogue, which a one-block-per-CU kernel cannot overlap with other
+  // work), both in microseconds, fitted to timings on MI355X at M = 2048,
+  // K = 4096 and 12288 (8B-shaped layers) and M = 65536, K = 768 and 3072
+  // (small layers).  Only the tiles of live rows count.  128 x 128 tiles run
+  // two blocks per CU (512 slots), the 4-wave kernel one (256 slots).  The
+  // 4-wave kernel may also split the columns: 256 x 256 tiles on the first
+  // c1, 256 x 128 tiles on the rest (one launch), so that each part fills
+  // whole waves of tiles (QKV at M = 2048: Q and K on 256 tiles, V on 256
+  // more, instead of three waves of 256 x 128 tiles).
   const int live = std::max(1, rows_hint >= 0 ? std::min(rows_hint, M) : M);
-  auto t_of = [&](int bm, int bn, long slots, double rate, long cols) -> double {
+  const int ei = (int)epi;
+  //                    fp32 store  residual  QKV   GELU  SwiGLU
+  static const double c0_128[5] = {9.3, 9.6, 5.9, 5.0, 5.0};
+  static const double c0_w128[5] = {10.6, 13.0, 8.5, 11.7, 11.7};
+  static const double c0_w256[5] = {21.5, 50.7, 18.3, 25.9, 7.0};
+  const double nk = (double)K / BK;
+  auto t_of = [&](int bm, int bn, long slots, double c0, double c1, long cols) -> double {
     if (cols <= 0) return 0.0;
-    const long tm = ceil_div(live, bm), tiles = tm * (long)ceil_div((int)cols, bn);
-    const double eff = (double)tiles / ((double)((tiles + slots - 1) / slots) * slots);
-    return (double)cols / (rate * live / ((double)tm * bm) * eff);
+    const long tiles = (long)ceil_div(live, bm) * ceil_div((int)cols, bn);
+    return (double)((tiles + slots - 1) / slots) * (c0 + nk * c1);
   };
-  const double t128 = t_of(128, 128, 512, 0.92, N);
+  const double t128 = t_of(128, 128, 512, c0_128[ei], 1.26, N);
   double t4 = 1e300;
   int split = -1;  // columns on 256 x 256 tiles
   // a QKV tile must lie inside one of Q, K, V: 256-wide tiles need d % 256 == 0
   const bool wide_ok = epi != EPI_QKV_ROPE || ea.d % 256 == 0;
   if (N % 128 == 0) {
     auto t_split = [&](int c1) {
-      return t_of(256, 256, 256, 1.23, c1) + t_of(256, 128, 256, 1.10, N - c1);
+      return t_of(256, 256, 256, c0_w256[ei], 1.53, c1) + t_of(256, 128, 256, c0_w128[ei], 0.98, N - c1);
     };
     // one tile shape (all 256 x 128, or all 256 x 256), then a split if it
     // is more than 3% faster (the estimate rounds each part up to whole

@@ -67,6 +67,10 @@ void embed(hipStream_t st, const int32_t* state, const void* table, int dtype, f
 void norm_rows(hipStream_t st, const float* x, void* out, int out_dtype, int n_rows, int d,
                int norm_kind, float eps, const int32_t* gather_rows, const int32_t* n_dev);
 void fill_i32(hipStream_t st, int32_t* p, int32_t v, size_t n);
+// dst[b*m_max + j] = src[sel_row[b*m_max + j]] (rows of d bf16) and
+// dst_mx[b*m_max + j] = mx[sel_row[b*m_max + j]] for j < n_sel[b], else zeros
+void gather_slot_rows(hipStream_t st, const bf16_t* src, const float* mx, const int32_t* sel_row,
+                      const int32_t* n_sel, int B, int m_max, int d, bf16_t* dst, float* dst_mx);
 
 // ---------------------------------------------------------------- coding stages
 // rows[] = flat indices b*T+t with state == mask_id (ascending), n_rows[0],

@@ -53,6 +53,8 @@ void dlmc_model::ensure_sel(int m_max) {
   dfree(sym);
   dfree(slot_base);
   dfree(cdf_ws);
+  dfree(slot_rows);
+  dfree(slot_mx);
   const size_t slots = (size_t)cfg.max_batch * m_max;
   sel_pos = (int32_t*)dalloc(slots * 4, true);
   sel_row = (int32_t*)dalloc(slots * 4, true);
@@ -62,6 +64,11 @@ void dlmc_model::ensure_sel(int m_max) {
   sym = (uint32_t*)dalloc(slots * 8, true);
   slot_base = (int64_t*)dalloc((size_t)cfg.max_batch * 8, true);
   cdf_ws = dalloc(cdf_workspace_bytes(slots, cfg.vocab));
+  slot_rows = (int32_t*)dalloc(slots * 4);
+  slot_mx = (float*)dalloc(slots * 4, true);
+  std::vector<int32_t> iota(slots);
+  for (size_t i = 0; i < slots; ++i) iota[i] = (int32_t)i;
+  DLMC_HIP(hipMemcpy(slot_rows, iota.data(), slots * 4, hipMemcpyHostToDevice));
   sel_cap = m_max;
 }
 
@@ -305,6 +312,7 @@ void dlmc_model::forward(const int32_t* st_dev, int B, int T, float* logits_out,
   const int timed_layer =
       prof && prof_one_layer ? (int)(prof_fwd++ % (uint64_t)layers.size()) : -1;
   prof_gated = false;
+  head_deferred = false;
 
   {
     StageTimer t(this, DLMC_STAGE_EMBED, Md * dd * (es + 4.0));
@@ -428,8 +436,21 @@ void dlmc_model::forward(const int32_t* st_dev, int B, int T, float* logits_out,
     norm_rows(s, x, hm, cfg.dtype, M, d, cfg.norm_kind, cfg.norm_eps, rw, nr);
   }
   if (inject_nan) poison_head_input(s, hm, bf16 ? 1 : 0, nr);
+  // Deferred logits: when writing the fp32 logits of every masked row would
+  // take longer than a second read of the head's weights for the committed
+  // rows (about 6 TB/s for the stores, 5 TB/s for the weights, 1 PFLOP/s),
+  // the head writes only the entropy statistics and selected_logits()
+  // computes the committed rows' logits after the selection.  A row's
+  // logits do not depend on the other rows of a launch, so both give the
+  // same bits.
+  if (bf16 && !logits_out && !rows_given && head_slots > 0 && head_slots <= max_rows &&
+      rows_hint > 0 && head_mode != 2) {
+    const double Vd = V, store_us = (double)rows_hint * Vd * 4.0 / 6.0e6;
+    const double redo_us = Vd * dd * es / 5.0e6 + 2.0 * head_slots * Vd * dd / 1.0e9 + 30.0;
+    head_deferred = head_mode == 1 || store_us > redo_us;
+  }
   EpiArgs o;
-  o.out = lg;
+  o.out = head_deferred ? nullptr : lg;
   o.ldo = V;
   o.stats = stats;  // the entropy's group statistics, fused into the head's epilogue
   o.stat_ld = stat_groups(V);
@@ -439,6 +460,19 @@ void dlmc_model::forward(const int32_t* st_dev, int B, int T, float* logits_out,
               rows_hint >= 0 ? (int)rows_hint : -1);
   else
     gemm_f32(s, (const float*)hm, (const float*)this->head, M, V, d, nr, EPI_STORE_F32, o);
+}
+
+void dlmc_model::selected_logits(int B, int m_max) {
+  if (!head_deferred) return;
+  const int d = cfg.d_model, V = cfg.vocab, n = B * m_max;
+  // h is free once the forward is done: the committed rows' inputs and row
+  // maxima, in slot order (empty slots zero)
+  gather_slot_rows(stream, (const bf16_t*)hm, mx, sel_row, n_sel, B, m_max, d, (bf16_t*)h, slot_mx);
+  EpiArgs o;
+  o.out = logits;
+  o.ldo = V;
+  StageTimer t(this, DLMC_STAGE_HEAD, 2.0 * n * (double)V * d);
+  gemm_bf16(stream, (const bf16_t*)h, (const bf16_t*)head, n, V, d, nullptr, EPI_STORE_F32, o);
 }
 
 void dlmc_model::row_stats(int n_max) {

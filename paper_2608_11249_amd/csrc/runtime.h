@@ -50,11 +50,19 @@ struct dlmc_model {
   uint32_t *cdf = nullptr, *sym = nullptr;
   void* cdf_ws = nullptr;  // segment partials of the CDF kernels
   int64_t* slot_base = nullptr;
+  int32_t* slot_rows = nullptr;  // slot_rows[i] = i: logits stored in slot order
+  float* slot_mx = nullptr;      // row max of selection slot i (deferred head)
   int32_t* tokens_dev = nullptr;
   size_t tokens_cap = 0;
 
   void* scratch = nullptr;  // this device's copy of the library's static scratch
   bool inject_nan = false;  // test hook: a NaN into the first logit of every forward
+  // Deferred logits.  head_slots (set by the caller of forward, 0 = never):
+  // the selection slots whose logits a deferred head would recompute;
+  // head_mode: 0 chooses by cost, 1 always defers, 2 never (test hook).
+  // head_deferred: the last forward wrote only the entropy statistics.
+  int head_slots = 0, head_mode = 0;
+  bool head_deferred = false;
   dlmc_trace_fn trace = nullptr;
   void* trace_user = nullptr;
 
@@ -101,6 +109,14 @@ struct dlmc_model {
   // the last forward into H / mx: merged from the head's group statistics
   // (bf16), or from the stored logits (fp32); both give the same bits
   void row_stats(int n_max);
+  // after a deferred head: the logits of the committed rows (sel_row /
+  // n_sel, B chunks of m_max slots) into logits, in slot order
+  void selected_logits(int B, int m_max);
+  // row index of selection slot i in logits: sel_row, or the slot itself
+  // after a deferred head
+  const int32_t* logit_rows() const { return head_deferred ? slot_rows : sel_row; }
+  // the row maxima the CDF reads at logit_rows()
+  const float* logit_max() const { return head_deferred ? slot_mx : mx; }
 };
 
 namespace dlmc {

@@ -298,7 +298,9 @@ int dlmc_session::step(uint64_t* coded) {
   for (int b = 0; b < B; ++b)
     if (slot_chunk[b] >= 0) masked += slot_left[b];
   if (cp.schedule == DLMC_SCHED_ENTROPY) {
+    m->head_slots = B * mm;  // the head may leave the logits to selected_logits()
     m->forward(m->state, B, T, nullptr, nullptr, nullptr, masked);
+    m->head_slots = 0;
     {
       StageTimer t(m, DLMC_STAGE_ENTROPY, m->bf16 ? (double)masked * stat_groups(V) * sizeof(RowStat)
                                                   : (double)masked * V * 4.0);
@@ -309,6 +311,7 @@ int dlmc_session::step(uint64_t* coded) {
       select_positions(s, m->H, m->rows, m->chunk_off, m->chunk_cnt, B, T, cp.tau_bits, cp.m_min, mm,
                        m->sel_pos, m->sel_row, m->n_sel, m->err);
     }
+    m->selected_logits(B, mm);
   } else {
     // the next block of each slot's masked positions, in ascending order
     int r = 0;
@@ -344,7 +347,7 @@ int dlmc_session::step(uint64_t* coded) {
     {
       // work (read the row once, write the CDF) is filled in once n_sel is known
       StageTimer t(m, DLMC_STAGE_CDF, 0.0);
-      cdf_rows(s, m->logits, m->mx, m->sel_row, m->n_sel, B, mm, V, P, m->cdf, nullptr, m->cdf_ws);
+      cdf_rows(s, m->logits, m->logit_max(), m->logit_rows(), m->n_sel, B, mm, V, P, m->cdf, nullptr, m->cdf_ws);
     }
     if (encode) {
       StageTimer t(m, DLMC_STAGE_REVEAL, 0.0);
@@ -353,7 +356,7 @@ int dlmc_session::step(uint64_t* coded) {
     }
   } else if (encode) {
     StageTimer t(m, DLMC_STAGE_REVEAL, 0.0);
-    rank_symbols(s, m->logits, m->sel_row, m->sel_pos, m->n_sel, m->tokens_dev, m->slot_base,
+    rank_symbols(s, m->logits, m->logit_rows(), m->sel_pos, m->n_sel, m->tokens_dev, m->slot_base,
                  m->state, B, T, mm, V, m->sym);
   }
   DLMC_HIP(hipMemcpyAsync(h_nsel, m->n_sel, (size_t)B * 4, hipMemcpyDeviceToHost, s));
@@ -389,7 +392,7 @@ int dlmc_session::step(uint64_t* coded) {
     DLMC_HIP(hipMemcpyAsync(m->dec, h_dec, (size_t)B * mm * 4, hipMemcpyHostToDevice, s));
     {
       StageTimer t(m, DLMC_STAGE_REVEAL, 0.0);
-      select_by_rank(s, m->logits, m->sel_row, m->sel_pos, m->n_sel, m->dec, m->state, B, T, mm, V);
+      select_by_rank(s, m->logits, m->logit_rows(), m->sel_pos, m->n_sel, m->dec, m->state, B, T, mm, V);
     }
     DLMC_HIP(hipMemcpyAsync(h_dec, m->dec, (size_t)B * mm * 4, hipMemcpyDeviceToHost, s));
     DLMC_HIP(hipStreamSynchronize(s));

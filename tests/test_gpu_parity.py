@@ -568,3 +568,39 @@ def test_fused_head_statistics_equal_standalone(kw, T, V):
             got = np.array([H[row_of[q]] for q in pos], dtype=np.float32)
             assert np.array_equal(got, np.array(ent, dtype=np.float32)), p
             state[pos] = toks[pos]
+
+
+@pytest.mark.parametrize("kw,cd,n", [
+    # 256 x 256 head tiles over the masked rows, 128 x 128 for the few slots
+    (dict(d_model=128, n_heads=1, d_ffn=256, vocab=98304), codec(600, k=16, P=24, W=64, batch=2), 1500),
+    # 0.5-bit threshold rule (1 to 64 per pass), three chunks per forward
+    (dict(ffn="swiglu", norm="rmsnorm"), codec(200, tau=0.5, mmin=1, mmax=64, P=24, W=64, batch=3), 700),
+    # symbol ranking reads the logits by slot too
+    (dict(vocab=3000), codec(128, k=8, batch=2, coder="rank"), 400),
+])
+def test_deferred_head_logits_same_containers(kw, cd, n):
+    """The LM head may store only the entropy statistics and leave the logits
+    of the committed rows to a second, smaller product after the selection.
+    Forcing that path on every pass, or forcing the full store, must give
+    byte-identical containers and identical traces (positions, entropies,
+    coded intervals, CDF hashes), and each container must decode under the
+    other mode."""
+    sh = shape(**kw)
+    toks = wl.markov1_tokens(n, sh.vocab, 21)
+    log("deferred head logits", kw, cd)
+    out = {}
+    with dl.Model(sh, max_chunk=cd.chunk_len, max_batch=cd.batch) as m:
+        for mode in (1, 2):
+            traces, tr = trace_recorder()
+            m.head_logits_mode(mode)
+            m.set_trace(tr, coded=True)
+            data = m.encode(toks, cd)
+            m.head_logits_mode(3 - mode)
+            back = m.decode(data)
+            m.set_trace(None)
+            assert np.array_equal(back, toks)
+            assert traces[0] == traces[1]
+            out[mode] = (data, traces[0])
+        m.head_logits_mode(0)
+    assert out[1][0] == out[2][0]
+    assert out[1][1] == out[2][1]
