@@ -1,9 +1,11 @@
 """GPU checks of the five workload configurations at their real model shapes.
 
 Round trips use a prefix of each workload's seeded stream (whole chunks, in
-the workload's chunk length and schedule); batch sizes are reduced where a
-full batch would not fit a test's time budget -- the kernels are batch
-invariant, which test_gpu_parity checks separately.  Logits of the 8B-shaped
+the workload's chunk length and schedule).  The small workload runs its full
+batch of 64 chunks; the 8B-shaped ones run reduced batches (8 of 32 chunks
+under the 0.5-bit rule, 1 of 4 long chunks), where a full batch would not fit
+a test's time budget -- the kernels are batch invariant, which test_gpu_parity
+checks separately.  Logits of the 8B-shaped
 model are compared with the oracle at full width with one layer (the launch
 shapes of every kernel are those of the 32-layer model), on a sample of
 vocabulary columns.
@@ -63,7 +65,8 @@ def roundtrip_workload(name, n_chunks, batch=None, trace=False):
 
 
 def test_roundtrip_small_config():
-    roundtrip_workload("small", 4, batch=4)
+    # the full batch: 64 chunks of 1024 tokens per forward, one batch
+    roundtrip_workload("small", 64, trace=True)
 
 
 def test_roundtrip_8b_config():
@@ -73,14 +76,16 @@ def test_roundtrip_8b_config():
 def test_roundtrip_8b_threshold_schedule():
     # tau = 0.5 bits, 1..64 positions per pass; report the pass count
     w = wl.WORKLOADS["8b-throughput"]
-    cd = dataclasses.replace(w.codec, batch=2)
-    toks = wl.make_tokens(w, 2 * cd.chunk_len)
+    nb = 8
+    cd = dataclasses.replace(w.codec, batch=nb)
+    toks = wl.make_tokens(w, nb * cd.chunk_len)
+    log("8b-throughput round trip", f"{nb} chunks x {cd.chunk_len}, batch {nb}")
     traces = {0: {}, 1: {}}
 
     def tr(d, chunk, pas, pos, ent, coded, h):
         traces[d][(chunk, pas)] = (tuple(pos), tuple(ent), tuple(coded), h)
 
-    with dl.Model(w.model, max_chunk=cd.chunk_len, max_batch=2) as m:
+    with dl.Model(w.model, max_chunk=cd.chunk_len, max_batch=nb) as m:
         m.set_trace(tr, coded=True)
         data = m.encode(toks, cd)
         back = m.decode(data)
@@ -89,7 +94,7 @@ def test_roundtrip_8b_threshold_schedule():
     # encode and decode took bit-identical decisions under the 0.5-bit rule
     assert traces[0] == traces[1]
     counts = [(c, len(t[0])) for (c, _), t in traces[0].items()]
-    per_chunk = [sum(1 for c, _ in counts if c == k) for k in range(2)]
+    per_chunk = [sum(1 for c, _ in counts if c == k) for k in range(nb)]
     assert all(1 <= n <= 64 for _, n in counts)
     # every pass commits all positions at or under 0.5 bits (capped at 64),
     # at least one
