@@ -620,6 +620,10 @@ gemm_bf16_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ Bw, in
   }
   if constexpr (StagedEpi<BM, BN, EPI>::enabled)
     epilogue_staged<BM, BN, EPI, BM / 2, BN / 2, 256>(acc, smem, m0, n0, wm, wn, tid, Mv, N, ea);
+  else if constexpr ((EPI == EPI_STORE_F32 || EPI == EPI_RESIDUAL) &&
+                     BM / 2 * (BN + 8) * 4 <= StagedEpi<BM, BN, EPI>::smem_elems * 2)
+    // an fp32 tile too large for the main loop's LDS, staged in two row halves
+    epilogue_store_halves<EPI, BM, BN, BM / 2, BN / 2, 256>(acc, smem, m0, n0, wm, wn, tid, Mv, N, ea);
   else
     epilogue<BM, BN, EPI>(acc, m0, n0, wm, wn, lane, Mv, N, ea);
 }
@@ -989,8 +993,10 @@ void gemm_bf16(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, i
   // and epilogue, which a one-block-per-CU kernel cannot overlap with other
   // work), both in microseconds, fitted to timings on MI355X at M = 2048,
   // K = 4096 and 12288 (8B-shaped layers) and M = 65536, K = 768 and 3072
-  // (small layers).  Only the tiles of live rows count.  128 x 128 tiles run
-  // two blocks per CU (512 slots), the 4-wave kernel one (256 slots).  The
+  // (small layers).  Only the tiles of live rows count.  128 x 128 and
+  // 192 x 128 tiles run two blocks per CU (512 slots), so one block's
+  // epilogue overlaps the other's main loop; the 4-wave kernel one (256
+  // slots).  The
   // 4-wave kernel may also split the columns: 256 x 256 tiles on the first
   // c1, 256 x 128 tiles on the rest (one launch), so that each part fills
   // whole waves of tiles (QKV at M = 2048: Q and K on 256 tiles, V on 256
@@ -1001,6 +1007,7 @@ void gemm_bf16(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, i
   static const double c0_128[5] = {9.3, 9.6, 5.9, 5.0, 5.0};
   static const double c0_w128[5] = {10.6, 13.0, 8.5, 11.7, 11.7};
   static const double c0_w256[5] = {21.5, 50.7, 18.3, 25.9, 7.0};
+  static const double c0_192[5] = {17.9, 20.5, 9.0, 9.7, 5.0};
   const double nk = (double)K / BK;
   auto t_of = [&](int bm, int bn, long slots, double c0, double c1, long cols) -> double {
     if (cols <= 0) return 0.0;
@@ -1008,6 +1015,8 @@ void gemm_bf16(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, i
     return (double)((tiles + slots - 1) / slots) * (c0 + nk * c1);
   };
   const double t128 = t_of(128, 128, 512, c0_128[ei], 1.26, N);
+  // 192 x 128: QKV tiles must lie inside Q, K or V (d % 128 == 0 holds)
+  const double t192 = t_of(192, 128, 512, c0_192[ei], 1.253, N);
   double t4 = 1e300;
   int split = -1;  // columns on 256 x 256 tiles
   // a QKV tile must lie inside one of Q, K, V: 256-wide tiles need d % 256 == 0
@@ -1033,7 +1042,9 @@ void gemm_bf16(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, i
       }
     }
   }
-  if (split >= 0 && t4 <= t128) {
+  if (t192 < t128 && (split < 0 || t192 < t4)) {
+    launch<192, 128>(st, A, B, M, N, K, M_dev, epi, ea);
+  } else if (split >= 0 && t4 <= t128) {
     if (split > 0 && split < N) {
       launch_split(st, A, B, M, N, K, M_dev, epi, ea, split);
     } else {

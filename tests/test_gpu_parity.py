@@ -391,6 +391,21 @@ def test_roundtrip_batch_invariance_attention_block_size():
     assert payloads(a) == payloads(b)
 
 
+def test_roundtrip_batch_invariance_192_row_tiles():
+    """One layer of the small model's shape, 32 chunks of 1024: with batch 32
+    (32768 rows) QKV and the GELU FFN-in run on 192 x 128 tiles, two blocks
+    per CU, whose row tiles straddle chunk boundaries; with batch 1 (1024
+    rows) they run on 128 x 128 tiles.  The payloads must not change."""
+    sh = shape(d_model=768, n_heads=12, d_ffn=3072, n_layers=1, vocab=384)
+    cd = codec(1024, k=64, batch=32)
+    toks = wl.markov1_tokens(32 * 1024, sh.vocab, 15)
+    log("batch invariance, 192 x 128 tiles")
+    with dl.Model(sh, max_chunk=1024, max_batch=32) as m:
+        a = roundtrip(m, toks, cd, batch_dec=1)
+        b = m.encode(toks, cd, batch=1)
+    assert payloads(a) == payloads(b)
+
+
 @pytest.mark.parametrize("kw,cd,n", [
     (dict(), codec(100, tau=4.0, mmin=1, mmax=8, batch=3), 350),
     (dict(ffn="swiglu", norm="rmsnorm", vocab=70000), codec(128, k=16, P=24, W=64, batch=2), 300),
