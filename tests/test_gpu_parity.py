@@ -619,3 +619,37 @@ def test_deferred_head_logits_same_containers(kw, cd, n):
         m.head_logits_mode(0)
     assert out[1][0] == out[2][0]
     assert out[1][1] == out[2][1]
+
+
+@pytest.mark.parametrize("n", [0, 1, 2, 31, 32, 33, 95])
+def test_roundtrip_edge_lengths(n):
+    """Inputs of 0, 1 and 2 tokens, one less than, exactly and one more than a
+    chunk, and a ragged tail after whole chunks (bf16 model, fixed k, batch
+    2): each round-trips bit-exactly, the empty input through an empty
+    container, and the decoder reports the stored length."""
+    sh = shape()
+    cd = codec(32, k=5, batch=2)
+    toks = wl.markov1_tokens(n, sh.vocab, 9)[:n] if n else np.zeros(0, dtype=np.int64)
+    log("edge length", n)
+    with dl.Model(sh, max_chunk=32, max_batch=2) as m:
+        data = m.encode(toks, cd)
+        assert dl.decode_size(data) == n
+        back = m.decode(data)
+    assert len(back) == n and np.array_equal(back, toks)
+
+
+def test_roundtrip_degenerate_inputs():
+    """A constant stream of the largest token id under fixed k, with every
+    masked position committed in the first pass (k above the chunk length),
+    and under the 0.5-bit rule; and a stream that alternates the smallest
+    and the largest ids.  All round-trip bit-exactly."""
+    sh = shape()
+    const = np.full(70, sh.vocab - 1, dtype=np.int64)
+    alt = np.where(np.arange(70) % 2 == 0, 0, sh.vocab - 1).astype(np.int64)
+    log("degenerate inputs")
+    with dl.Model(sh, max_chunk=32, max_batch=2) as m:
+        for toks in (const, alt):
+            for cd in (codec(32, k=4, batch=2), codec(32, k=64, batch=2),
+                       codec(32, tau=0.5, mmin=1, mmax=64, batch=2)):
+                data = m.encode(toks, cd)
+                assert np.array_equal(m.decode(data), toks), cd
