@@ -298,9 +298,15 @@ int dlmc_session::step(uint64_t* coded) {
   for (int b = 0; b < B; ++b)
     if (slot_chunk[b] >= 0) masked += slot_left[b];
   if (cp.schedule == DLMC_SCHED_ENTROPY) {
-    m->head_slots = B * mm;  // the head may leave the logits to selected_logits()
-    m->forward(m->state, B, T, nullptr, nullptr, nullptr, masked);
-    m->head_slots = 0;
+    {
+      // the head may leave the logits to selected_logits(); reset even if the forward throws
+      struct HeadSlots {
+        dlmc_model* m;
+        ~HeadSlots() { m->head_slots = 0; }
+      } reset{m};
+      m->head_slots = B * mm;
+      m->forward(m->state, B, T, nullptr, nullptr, nullptr, masked);
+    }
     {
       StageTimer t(m, DLMC_STAGE_ENTROPY, m->bf16 ? (double)masked * stat_groups(V) * sizeof(RowStat)
                                                   : (double)masked * V * 4.0);
