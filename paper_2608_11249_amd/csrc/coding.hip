@@ -398,6 +398,94 @@ __global__ void reveal_kernel(const int32_t* __restrict__ sel_pos, const int32_t
   }
 }
 
+// ---------------------------------------------------------------- decoding
+// One wave per slot.  Every lane keeps the same decoder state; the lanes only
+// split the search for the symbol, the largest s with row[s] <= t (row[0] = 0
+// <= t < 2^P = row[V]): each round probes 64 evenly spaced entries of the
+// bracket [lo, hi) and keeps the stretch after the last probe that is <= t,
+// so V + 1 = 126465 entries take three rounds of one load per lane.
+__global__ void __launch_bounds__(64)
+decode_symbols_kernel(const uint32_t* __restrict__ cdf, const int32_t* __restrict__ n_sel, int m_max,
+                      int V, int P, int W, int rans, uint64_t rans_lo, const uint8_t* __restrict__ payload,
+                      DecSlot* __restrict__ slots, int32_t* __restrict__ dec, uint32_t* __restrict__ iv,
+                      int32_t* __restrict__ err) {
+  const int b = blockIdx.x, lane = threadIdx.x;
+  DecSlot d = slots[b];
+  if (!d.live) return;
+  const int ns = min(n_sel[b], m_max);
+  const uint8_t* data = payload + d.off;
+  const uint64_t total = 1ull << P;
+  bool bad = false;
+  for (int j = 0; j < ns; ++j) {
+    const int slot = b * m_max + j;
+    const uint32_t* row = cdf + (size_t)slot * ((size_t)V + 1);
+    uint64_t r = 0, t;
+    if (rans) {
+      t = d.x & (total - 1);
+    } else {
+      r = d.range >> P;
+      if (r == 0) {
+        bad = true;
+        break;
+      }
+      t = d.x / r;
+      if (t >= total) {
+        bad = true;
+        break;
+      }
+    }
+    int lo = 0, hi = V;
+    for (int round = 0; round < 8 && hi - lo > 1; ++round) {
+      const int step = (hi - lo + 63) / 64;
+      const int idx = lo + lane * step;
+      const uint64_t le = __ballot(idx < hi && (uint64_t)row[idx] <= t);
+      if (!le) break;  // row[lo] > t: not a CDF row; caught below
+      lo += (63 - __clzll(le)) * step;
+      hi = min(lo + step, hi);
+    }
+    const uint32_t c0 = row[lo], c1 = row[lo + 1];
+    if (hi - lo != 1 || c0 > t || c1 <= t) {
+      bad = true;
+      break;
+    }
+    const uint64_t f = c1 - c0;
+    if (rans) {
+      d.x = f * (d.x >> P) + t - c0;
+      while (d.x < rans_lo) {
+        if (d.pos + 4 > d.len) {
+          bad = true;
+          break;
+        }
+        const uint8_t* w = data + d.pos;
+        d.x = (d.x << 32) | ((uint64_t)w[0] | (uint64_t)w[1] << 8 | (uint64_t)w[2] << 16 | (uint64_t)w[3] << 24);
+        d.pos += 4;
+      }
+      if (bad) break;
+    } else {
+      d.x -= r * c0;
+      d.range = r * f;
+      const uint64_t lim = 1ull << (W - 8);
+      while (d.range < lim) {
+        d.x = (d.x << 8) | (d.pos < d.len ? data[d.pos] : 0u);
+        ++d.pos;
+        d.range <<= 8;
+      }
+    }
+    if (lane == 0) {
+      dec[slot] = lo;
+      iv[2 * slot] = c0;
+      iv[2 * slot + 1] = (uint32_t)f;
+    }
+  }
+  if (lane == 0) {
+    if (bad) {
+      d.live = 0;
+      atomicCAS(err, 0, 2);
+    }
+    slots[b] = d;
+  }
+}
+
 }  // namespace
 
 void compact_masked(hipStream_t st, const int32_t* state, int B, int T, int mask_id,
@@ -482,6 +570,17 @@ void reveal(hipStream_t st, const int32_t* sel_pos, const int32_t* n_sel, const 
             int32_t* state, int B, int T, int m_max) {
   if (B <= 0) return;
   reveal_kernel<<<B, 256, 0, st>>>(sel_pos, n_sel, dec, state, T, m_max);
+  DLMC_HIP(hipGetLastError());
+}
+
+void decode_symbols(hipStream_t st, const uint32_t* cdf, const int32_t* n_sel, int B, int m_max,
+                    int V, int P, int W, bool rans, uint64_t rans_lo, const uint8_t* payload,
+                    DecSlot* slots, int32_t* dec, uint32_t* iv, int32_t* err) {
+  if (B <= 0) return;
+  DLMC_CHECK(V >= 1 && P >= 1 && P <= 31 && (rans || (W >= 16 && W <= 64 && P <= W - 16)), DLMC_E_INVAL,
+             "decode_symbols: bad coder parameters");
+  decode_symbols_kernel<<<B, 64, 0, st>>>(cdf, n_sel, m_max, V, P, W, rans ? 1 : 0, rans_lo, payload,
+                                          slots, dec, iv, err);
   DLMC_HIP(hipGetLastError());
 }
 

@@ -118,6 +118,23 @@ void gather_reveal(hipStream_t st, const uint32_t* cdf, const int32_t* sel_pos,
 // decode: reveal decoded symbols
 void reveal(hipStream_t st, const int32_t* sel_pos, const int32_t* n_sel, const int32_t* dec,
             int32_t* state, int B, int T, int m_max);
+// decode: the entropy decoder of one batch slot, kept in device memory between
+// passes.  Range coder: x = code - low and range; rANS: x = the state.  pos /
+// len: read position and length (bytes) of the slot's stream, which starts at
+// byte off of the payload buffer.  Slots with live = 0 decode nothing.
+struct DecSlot {
+  uint64_t x, range, pos, len, off;
+  uint32_t live, pad;
+};
+// decode: one wave per live slot b decodes the slot's n_sel[b] committed
+// symbols of the pass, in slot order, from CDF rows b * m_max + j (V + 1 words
+// each) with the arithmetic of the host decoders (W-bit range coder, or rANS
+// with lower bound rans_lo when `rans`); writes dec[slot] = symbol and
+// iv[2 slot], iv[2 slot + 1] = (start, freq), and the slot's new state.  A
+// corrupt stream stops its slot and sets *err to 2 if it was 0.
+void decode_symbols(hipStream_t st, const uint32_t* cdf, const int32_t* n_sel, int B, int m_max,
+                    int V, int P, int W, bool rans, uint64_t rans_lo, const uint8_t* payload,
+                    DecSlot* slots, int32_t* dec, uint32_t* iv, int32_t* err);
 // attention-based context: A[i, :] (+)= w softmax(scale S[i, :]) (rows T,
 // pitch T), and out = (A^T v + v) / 2
 void softmax_accumulate(hipStream_t st, const float* S, float* A, int T, float scale, float w,

@@ -96,6 +96,8 @@ class RangeDecoder {
     return s;
   }
   size_t consumed() const { return pos_; }
+  uint64_t code_minus_low() const { return D_; }
+  uint64_t range() const { return range_; }
 
  private:
   uint8_t next() { return pos_ < len_ ? data_[pos_++] : (++pos_, 0); }

@@ -87,6 +87,8 @@ class RansDecoder {
     return s;
   }
   bool done() const { return pos_ == len_ && x_ == RANS_L; }
+  uint64_t state() const { return x_; }
+  size_t position() const { return pos_; }
 
  private:
   const uint8_t* data_ = nullptr;

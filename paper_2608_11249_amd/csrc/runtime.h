@@ -195,6 +195,13 @@ struct dlmc_session {
   std::vector<const uint8_t*> rk_data;
   std::vector<size_t> rk_len, rk_pos;
   std::vector<int32_t> rk_rank;  // decode: the ranks of the current pass (trace)
+  // decode with the range coder or rANS: the payload section on the device,
+  // each chunk's offset in it, and the slots' decoder states (device, and the
+  // host copy of the last pass's)
+  uint8_t* d_payload = nullptr;
+  std::vector<uint64_t> pl_off;
+  dlmc::DecSlot* d_dslot = nullptr;
+  dlmc::DecSlot* h_dslot = nullptr;
   // initial context and left-to-right block schedules
   std::vector<std::vector<int32_t>> slot_ctx_pos, slot_ctx_sym;  // per slot
   std::vector<std::vector<int32_t>> slot_order;  // masked positions, ascending
@@ -208,7 +215,7 @@ struct dlmc_session {
   int32_t* h_pos = nullptr;
   int32_t* h_err = nullptr;
   uint32_t* h_sym = nullptr;
-  uint32_t* h_cdf = nullptr;  // decode / trace: sel_cap * (V+1) per slot
+  uint32_t* h_cdf = nullptr;  // trace: sel_cap * (V+1) per slot
   int32_t* h_dec = nullptr;
   int64_t* h_base = nullptr;
   int32_t* h_state = nullptr;   // max_batch * max_chunk: a slot's initial state

@@ -160,6 +160,11 @@ dlmc_session::~dlmc_session() {
   (void)hipHostFree(h_selpos);
   (void)hipHostFree(h_selrow);
   (void)hipHostFree(h_nsel_up);
+  (void)hipHostFree(h_dslot);
+  if (m) {
+    m->dfree(d_payload);
+    m->dfree(d_dslot);
+  }
 }
 
 void dlmc_session::assign(int b, uint64_t chunk) {
@@ -208,10 +213,26 @@ void dlmc_session::assign(int b, uint64_t chunk) {
       rk_data[b] = data;
       rk_len[b] = len;
       rk_pos[b] = 0;
-    } else if (rans) {
-      if (!rdecs[b].reset(data, len, P)) throw Error(DLMC_E_CORRUPT, "not an rANS stream");
     } else {
-      decs[b].reset(data, len, cp.coder_bits, P);
+      // the stream's initial state (host decoder), then the pass-by-pass
+      // decoding on the device
+      DecSlot& d = h_dslot[b];
+      if (rans) {
+        if (!rdecs[b].reset(data, len, P)) throw Error(DLMC_E_CORRUPT, "not an rANS stream");
+        d.x = rdecs[b].state();
+        d.range = 0;
+        d.pos = rdecs[b].position();
+      } else {
+        decs[b].reset(data, len, cp.coder_bits, P);
+        d.x = decs[b].code_minus_low();
+        d.range = decs[b].range();
+        d.pos = decs[b].consumed();
+      }
+      d.len = len;
+      d.off = pl_off[chunk] + 6 * (size_t)c;
+      d.live = 1;
+      d.pad = 0;
+      DLMC_HIP(hipMemcpyAsync(d_dslot + b, &d, sizeof(DecSlot), hipMemcpyHostToDevice, m->stream));
     }
   }
   slot_left[b] = T - c;
@@ -359,6 +380,13 @@ int dlmc_session::step(uint64_t* coded) {
       StageTimer t(m, DLMC_STAGE_REVEAL, 0.0);
       gather_reveal(s, m->cdf, m->sel_pos, m->n_sel, m->tokens_dev, m->slot_base, m->state, B, T, mm,
                     V, m->sym);
+    } else {
+      StageTimer t(m, DLMC_STAGE_REVEAL, 0.0);
+      decode_symbols(s, m->cdf, m->n_sel, B, mm, V, P, cp.coder_bits, cp.coder == DLMC_CODER_RANS, RANS_L,
+                     d_payload, d_dslot, m->dec, m->sym, m->err);
+      reveal(s, m->sel_pos, m->n_sel, m->dec, m->state, B, T, mm);
+      DLMC_HIP(hipMemcpyAsync(h_dec, m->dec, (size_t)B * mm * 4, hipMemcpyDeviceToHost, s));
+      DLMC_HIP(hipMemcpyAsync(h_dslot, d_dslot, (size_t)B * sizeof(DecSlot), hipMemcpyDeviceToHost, s));
     }
   } else if (encode) {
     StageTimer t(m, DLMC_STAGE_REVEAL, 0.0);
@@ -368,8 +396,9 @@ int dlmc_session::step(uint64_t* coded) {
   DLMC_HIP(hipMemcpyAsync(h_nsel, m->n_sel, (size_t)B * 4, hipMemcpyDeviceToHost, s));
   DLMC_HIP(hipMemcpyAsync(h_pos, m->sel_pos, (size_t)B * mm * 4, hipMemcpyDeviceToHost, s));
   DLMC_HIP(hipMemcpyAsync(h_err, m->err, 4, hipMemcpyDeviceToHost, s));
-  if (encode) DLMC_HIP(hipMemcpyAsync(h_sym, m->sym, (size_t)B * mm * 8, hipMemcpyDeviceToHost, s));
+  if (encode || !rank) DLMC_HIP(hipMemcpyAsync(h_sym, m->sym, (size_t)B * mm * 8, hipMemcpyDeviceToHost, s));
   DLMC_HIP(hipStreamSynchronize(s));
+  if (*h_err == 2) throw Error(DLMC_E_CORRUPT, "decoder target out of range");
   if (*h_err) throw Error(DLMC_E_NUMERIC, "non-finite entropy (non-finite logits)");
   if (cdf_rec < m->prof_recs.size() && m->prof_recs[cdf_rec].stage == DLMC_STAGE_CDF) {
     int64_t committed = 0;
@@ -419,13 +448,12 @@ int dlmc_session::step(uint64_t* coded) {
     Hall.resize((size_t)top + 1);
     if (top >= 0) DLMC_HIP(hipMemcpy(Hall.data(), m->H, Hall.size() * 4, hipMemcpyDeviceToHost));
   }
-  bool any_dec = false;
   std::vector<uint32_t> coded_iv;  // trace: the pass's coded pairs of one slot
   for (int b = 0; b < B; ++b) {
     if (slot_chunk[b] < 0) continue;
     const int ns = h_nsel[b];
     const uint32_t* rows_cdf = nullptr;
-    if (!rank && (!encode || m->trace)) {
+    if (!rank && m->trace) {
       DLMC_HIP(hipMemcpy(h_cdf, m->cdf + (size_t)b * mm * row_words, (size_t)ns * row_words * 4,
                          hipMemcpyDeviceToHost));
       rows_cdf = h_cdf;
@@ -460,14 +488,10 @@ int dlmc_session::step(uint64_t* coded) {
         if (cp.coder == DLMC_CODER_RANS) rencs[b].encode(st, fr);
         else encs[b].encode(st, fr);
       } else {
-        const uint32_t* cdf_j = rows_cdf + (size_t)j * row_words;
-        const int sym = cp.coder == DLMC_CODER_RANS ? rdecs[b].decode(cdf_j, V) : decs[b].decode(cdf_j, V);
-        if (sym < 0) throw Error(DLMC_E_CORRUPT, "decoder target out of range");
-        tokens[base + pos] = sym;
-        h_dec[b * mm + j] = sym;
-        coded_iv[2 * j] = cdf_j[sym];
-        coded_iv[2 * j + 1] = cdf_j[sym + 1] - cdf_j[sym];
-        any_dec = true;
+        // decoded on the device
+        tokens[base + pos] = h_dec[b * mm + j];
+        coded_iv[2 * j] = h_sym[2 * (b * mm + j)];
+        coded_iv[2 * j + 1] = h_sym[2 * (b * mm + j) + 1];
       }
     }
     if (m->trace) {
@@ -484,10 +508,6 @@ int dlmc_session::step(uint64_t* coded) {
     slot_cursor[b] += ns;
     DLMC_CHECK(slot_left[b] >= 0 && (ns > 0 || slot_left[b] == 0), DLMC_E_CORRUPT,
                "schedule committed no position");
-  }
-  if (!encode && any_dec) {
-    DLMC_HIP(hipMemcpyAsync(m->dec, h_dec, (size_t)B * mm * 4, hipMemcpyHostToDevice, s));
-    reveal(s, m->sel_pos, m->n_sel, m->dec, m->state, B, T, mm);
   }
   ++passes;
 
@@ -513,7 +533,7 @@ int dlmc_session::step(uint64_t* coded) {
         }
         if (!body.empty()) std::memcpy(pl.data() + 6 * c, body.data(), body.size());
         payload[chunk] = std::move(pl);
-      } else if (cp.coder == DLMC_CODER_RANS && !rdecs[b].done()) {
+      } else if (cp.coder == DLMC_CODER_RANS && !(h_dslot[b].pos == h_dslot[b].len && h_dslot[b].x == RANS_L)) {
         throw Error(DLMC_E_CORRUPT, "rANS stream did not end in its initial state");
       } else if (cp.coder == DLMC_CODER_RANK && rk_pos[b] != rk_len[b]) {
         throw Error(DLMC_E_CORRUPT, "rank stream has trailing data");
@@ -529,6 +549,10 @@ int dlmc_session::step(uint64_t* coded) {
       } else {
         slot_chunk[b] = -1;
         fill_i32(s, m->state + (size_t)b * T, 0, (size_t)T);
+        if (!encode && !rank) {
+          h_dslot[b].live = 0;
+          DLMC_HIP(hipMemcpyAsync(d_dslot + b, h_dslot + b, sizeof(DecSlot), hipMemcpyHostToDevice, s));
+        }
       }
       base_changed = true;
     }
@@ -776,6 +800,16 @@ dlmc_session* make_decoder(dlmc_model* m, const uint8_t* in, uint64_t len, int32
   s->end_chunk = ci.n_chunks;
   s->tokens.assign(ci.n, 0);
   read_payloads(in, len, ci, s->payload, s->crc);
+  if (cp.coder != DLMC_CODER_RANK) {
+    // the payload section is the chunks' payloads back to back
+    s->pl_off.resize(ci.count + 1);
+    for (uint64_t c = 0; c <= ci.count; ++c) s->pl_off[c] = get<uint64_t>(in, FIXED_HEADER + c * 8);
+    s->d_payload = (uint8_t*)m->dalloc(ci.total);
+    if (ci.total) DLMC_HIP(hipMemcpy(s->d_payload, in + ci.hdr, ci.total, hipMemcpyHostToDevice));
+    s->d_dslot = (DecSlot*)m->dalloc((size_t)m->cfg.max_batch * sizeof(DecSlot), true);
+    pinned((void**)&s->h_dslot, (size_t)m->cfg.max_batch * sizeof(DecSlot));
+    std::memset(s->h_dslot, 0, (size_t)m->cfg.max_batch * sizeof(DecSlot));
+  }
   return s.release();
 }
 

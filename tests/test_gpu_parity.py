@@ -440,6 +440,51 @@ def test_errors_on_gpu_model():
         assert e.value.code == -4
 
 
+@pytest.mark.parametrize("coder,W", [("range", 32), ("range", 64), ("rans", 32)])
+def test_device_decoder_corrupt_streams(coder, W):
+    """The device decoders on damaged coded bytes (bf16 model, two chunks
+    decoded side by side).  A range stream whose first W/8 bytes are all ones
+    gives a first target of 2^P (code - low >= range) and is refused with
+    E_CORRUPT; so is an rANS stream whose final state is changed.  Random
+    single-byte damage in the payload section is refused with E_CORRUPT or
+    decodes: with the per-chunk CRC only to the original tokens, without it to
+    any tokens.  The same model then decodes the intact container."""
+    sh = shape()
+    cd = codec(32, k=4, batch=2, W=W, coder=coder)
+    toks = wl.markov1_tokens(100, sh.vocab, 5)
+    with dl.Model(sh, max_chunk=32, max_batch=2) as m:
+        for crc in (True, False):
+            data = m.encode(toks, cd, crc=crc)
+            hdr = int.from_bytes(data[8:12], "little")
+            offs = [int.from_bytes(data[144 + 8 * c: 152 + 8 * c], "little") for c in range(5)]
+            bad = bytearray(data)
+            s1 = hdr + offs[1]  # chunk 1's stream (no initial context)
+            if coder == "range":
+                bad[s1: s1 + W // 8] = b"\xff" * (W // 8)
+            else:
+                bad[s1 + 3] ^= 0x10  # a bit of the final state below 2^31
+            log("corrupt head of chunk 1", coder, W, crc)
+            with pytest.raises(dl.DlmcError) as e:
+                m.decode(bytes(bad))
+            assert e.value.code == -5
+            rng = np.random.default_rng(7 + W)
+            for trial in range(6):
+                bad = bytearray(data)
+                pos = int(rng.integers(hdr, len(data)))
+                bad[pos] ^= int(rng.integers(1, 256))
+                log("corrupt byte", coder, W, crc, pos)
+                try:
+                    back = m.decode(bytes(bad))
+                except dl.DlmcError as err:
+                    assert err.code == -5
+                else:
+                    assert len(back) == len(toks)
+                    if crc:
+                        assert np.array_equal(back, toks)
+            log("intact", coder, W, crc)
+            assert np.array_equal(m.decode(data), toks)
+
+
 def test_stage_profile_mask():
     """Only the stages named in the profile mask are timed; the CDF stage's
     work is filled in only when it is itself timed."""
