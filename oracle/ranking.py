@@ -13,10 +13,15 @@ varint: unsigned LEB128 -- 7 bits per byte, least significant group first,
 the high bit set on every byte but the last.
 
 Container-level compression: the concatenated chunk payloads are compressed as
-one block ("none", "zlib" at a level, "lzma" xz at a preset).
+one block ("none", "zlib" at a level, "lzma" xz at a preset, "zstd" at a
+level).  zlib and lzma come from Python's standard modules; zstd from the
+system's libzstd (ZSTD_compress / ZSTD_decompress, through ctypes), since no
+Python binding is installed.
 """
 from __future__ import annotations
 
+import ctypes
+import ctypes.util
 import lzma
 import zlib
 from typing import List
@@ -75,6 +80,62 @@ def varint_decode(data: bytes, n: int, pos: int = 0):
     return vals, pos
 
 
+_ZSTD = None
+
+
+def zstd_library():
+    """The system libzstd (ctypes), or None when it is not installed."""
+    global _ZSTD
+    if _ZSTD is None:
+        name = ctypes.util.find_library("zstd") or "libzstd.so.1"
+        try:
+            lib = ctypes.CDLL(name)
+        except OSError:
+            _ZSTD = False
+            return None
+        sz, vp, cvp = ctypes.c_size_t, ctypes.c_void_p, ctypes.c_void_p
+        lib.ZSTD_compressBound.restype = sz
+        lib.ZSTD_compressBound.argtypes = [sz]
+        lib.ZSTD_compress.restype = sz
+        lib.ZSTD_compress.argtypes = [vp, sz, cvp, sz, ctypes.c_int]
+        lib.ZSTD_decompress.restype = sz
+        lib.ZSTD_decompress.argtypes = [vp, sz, cvp, sz]
+        lib.ZSTD_getFrameContentSize.restype = ctypes.c_ulonglong
+        lib.ZSTD_getFrameContentSize.argtypes = [cvp, sz]
+        lib.ZSTD_isError.restype = ctypes.c_uint
+        lib.ZSTD_isError.argtypes = [sz]
+        _ZSTD = lib
+    return _ZSTD or None
+
+
+def _zstd_compress(data: bytes, level: int) -> bytes:
+    lib = zstd_library()
+    if lib is None:
+        raise RuntimeError("libzstd is not installed")
+    cap = lib.ZSTD_compressBound(len(data))
+    out = ctypes.create_string_buffer(max(cap, 1))
+    n = lib.ZSTD_compress(out, cap, bytes(data), len(data), level)
+    if lib.ZSTD_isError(n):
+        raise ValueError("zstd compression failed")
+    return out.raw[:n]
+
+
+def _zstd_decompress(blob: bytes) -> bytes:
+    """One zstd frame that states its content size (RFC 8878, Frame_Content_Size)."""
+    lib = zstd_library()
+    if lib is None:
+        raise RuntimeError("libzstd is not installed")
+    blob = bytes(blob)
+    size = lib.ZSTD_getFrameContentSize(blob, len(blob))
+    if size >= (1 << 64) - 2:  # unknown (2^64 - 1) or not a frame (2^64 - 2)
+        raise ValueError("not a zstd frame with a content size")
+    out = ctypes.create_string_buffer(max(size, 1))
+    n = lib.ZSTD_decompress(out, size, blob, len(blob))
+    if lib.ZSTD_isError(n) or n != size:
+        raise ValueError("corrupt zstd frame")
+    return out.raw[:n]
+
+
 def compress(data: bytes, kind: str, level: int) -> bytes:
     if kind == "none":
         return bytes(data)
@@ -82,6 +143,8 @@ def compress(data: bytes, kind: str, level: int) -> bytes:
         return zlib.compress(bytes(data), level)
     if kind == "lzma":
         return lzma.compress(bytes(data), format=lzma.FORMAT_XZ, preset=level)
+    if kind == "zstd":
+        return _zstd_compress(data, level)
     raise ValueError(kind)
 
 
@@ -92,4 +155,6 @@ def decompress(blob: bytes, kind: str) -> bytes:
         return zlib.decompress(blob)
     if kind == "lzma":
         return lzma.decompress(blob, format=lzma.FORMAT_XZ)
+    if kind == "zstd":
+        return _zstd_decompress(blob)
     raise ValueError(kind)

@@ -64,6 +64,7 @@ def section(container: bytes, kind: str):
     dict(schedule="uniform", blocks=32, m_min=1, m_max=8, rank_compressor="lzma", rank_level=9),
     dict(schedule="uniform", blocks=16, m_min=1, m_max=64, rank_compressor="zlib", rank_level=9,
          context=2, context_kind="random", context_seed=4),
+    dict(schedule="uniform", blocks=8, m_min=1, m_max=32, rank_compressor="zstd", rank_level=3),
 ])
 def test_tiny_ranks_against_oracle(kw):
     w = wl.WORKLOADS["tiny"]
@@ -103,7 +104,7 @@ def test_bf16_rank_roundtrip_and_batch_invariance(comp, level, sched):
         # identical apart from the header's default decode batch (bytes 72..75)
         assert a[:72] == b[:72] and a[76:] == b[76:]
         assert np.array_equal(m.decode(a, batch=2), toks)
-        if comp in ("zlib", "lzma"):
+        if comp in ("zlib", "lzma", "zstd"):
             assert section(a, comp)  # the section is a valid stream of that compressor
 
 

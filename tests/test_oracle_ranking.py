@@ -52,6 +52,53 @@ def test_compressor_roundtrip(kind, level):
         assert len(blob) < len(data)
 
 
+needs_zstd = pytest.mark.skipif(R.zstd_library() is None, reason="libzstd is not installed")
+
+
+def zstd_frame(blocks, content_size):
+    """A zstd frame written out from RFC 8878: magic 0xFD2FB528, a frame header
+    descriptor with only Single_Segment_flag set (so a one-byte
+    Frame_Content_Size follows, no window descriptor), then blocks, each a
+    3-byte little-endian header (bit 0 Last_Block, bits 1-2 Block_Type: 0 Raw,
+    1 RLE; bits 3-23 Block_Size) and its content."""
+    assert content_size < 256
+    out = bytearray((0xFD2FB528).to_bytes(4, "little")) + bytes([0x20, content_size])
+    for i, (kind, payload, size) in enumerate(blocks):
+        last = 1 if i == len(blocks) - 1 else 0
+        out += (last | (kind << 1) | (size << 3)).to_bytes(3, "little") + payload
+    return bytes(out)
+
+
+@needs_zstd
+def test_zstd_pinned_to_hand_built_frames():
+    """The oracle's zstd decoder against frames built from the format's
+    definition: a raw block, an RLE block, and a raw block followed by an RLE
+    block; a frame with a damaged magic number is refused."""
+    raw = bytes(range(7, 107))
+    assert R.decompress(zstd_frame([(0, raw, len(raw))], len(raw)), "zstd") == raw
+    assert R.decompress(zstd_frame([(1, b"\x2a", 200)], 200), "zstd") == b"\x2a" * 200
+    two = zstd_frame([(0, b"abc", 3), (1, b"z", 5)], 8)
+    assert R.decompress(two, "zstd") == b"abczzzzz"
+    bad = bytearray(two)
+    bad[0] ^= 1
+    with pytest.raises(ValueError):
+        R.decompress(bytes(bad), "zstd")
+
+
+@needs_zstd
+@pytest.mark.parametrize("level", [1, 19])
+def test_zstd_roundtrip_and_frame_header(level):
+    """Round trip at two levels; the frame starts with the magic number and
+    states its content size (Single_Segment_flag or a nonzero
+    Frame_Content_Size_flag), which the decoder needs."""
+    data = R.varint_encode(np.random.default_rng(2).geometric(0.3, size=5000))
+    blob = R.compress(data, "zstd", level)
+    assert blob[:4] == (0xFD2FB528).to_bytes(4, "little")
+    fhd = blob[4]
+    assert (fhd & 0x20) or (fhd >> 6)
+    assert R.decompress(blob, "zstd") == data and len(blob) < len(data)
+
+
 @pytest.mark.parametrize("kw", [
     dict(m_min=4, m_max=4),
     dict(schedule="uniform", blocks=6, context=3, context_kind="random", context_seed=2),
