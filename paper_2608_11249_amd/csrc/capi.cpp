@@ -206,10 +206,13 @@ dlmc_status dlmc_decode(dlmc_model* m, const uint8_t* in, uint64_t len, int32_t 
   dlmc_session* s = nullptr;
   dlmc_status st = guard([&] {
     use(m);
+    // the output size is checked from the header before any allocation
+    ContainerInfo ci;
+    parse_header(in, len, &ci);
+    if (n) *n = ci.n;
+    if (!tokens || cap < ci.n)
+      throw Error(DLMC_E_BUFFER, "token buffer too small: need " + std::to_string(ci.n));
     s = make_decoder(m, in, len, batch);
-    if (n) *n = s->n;
-    if (!tokens || cap < s->n)
-      throw Error(DLMC_E_BUFFER, "token buffer too small: need " + std::to_string(s->n));
     while (!s->step(nullptr)) {
     }
     if (s->n) std::memcpy(tokens, s->tokens.data(), s->n * 4);

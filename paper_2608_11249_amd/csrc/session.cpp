@@ -744,11 +744,21 @@ void parse_header(const uint8_t* in, uint64_t len, ContainerInfo* ci) {
   cp->reserved = 0;
   cp->context_seed = 0;  // positions are stored with each chunk
   DLMC_CHECK(cp->chunk_len >= 1, DLMC_E_FORMAT, "bad chunk length");
-  DLMC_CHECK(ci->n_chunks == (ci->n + cp->chunk_len - 1) / cp->chunk_len, DLMC_E_FORMAT, "bad chunk count");
+  DLMC_CHECK(cp->coder == DLMC_CODER_RANGE || cp->coder == DLMC_CODER_RANS || cp->coder == DLMC_CODER_RANK,
+             DLMC_E_FORMAT, "unknown coder");
+  DLMC_CHECK(cp->coder != DLMC_CODER_RANK || rank_compressor_ok(cp->rank_compressor, cp->rank_level),
+             DLMC_E_FORMAT, "bad rank compressor / level");
+  // every size below comes from the input: compared by division, or bounded
+  // by the buffer length first, so no sum or product can wrap
+  const uint64_t cl = (uint64_t)cp->chunk_len;
+  DLMC_CHECK(ci->n_chunks == ci->n / cl + (ci->n % cl != 0), DLMC_E_FORMAT, "bad chunk count");
   DLMC_CHECK(ci->first <= ci->n_chunks && ci->count <= ci->n_chunks - ci->first &&
                  (ci->count >= 1 || ci->n_chunks == 0),
              DLMC_E_FORMAT, "bad chunk range");
   const bool crc_on = cp->flags & DLMC_FLAG_CRC;
+  // count + 1 offsets (8 bytes each) and, with CRCs, count CRCs (4 bytes) fit
+  DLMC_CHECK(len >= FIXED_HEADER + 8 && ci->count <= (len - FIXED_HEADER - 8) / (crc_on ? 12 : 8),
+             DLMC_E_FORMAT, "bad header size");
   const uint64_t need = FIXED_HEADER + (ci->count + 1) * 8 + (crc_on ? ci->count * 4 : 0);
   DLMC_CHECK(ci->hdr == need && len >= need, DLMC_E_FORMAT, "bad header size");
   DLMC_CHECK(get<uint64_t>(in, FIXED_HEADER) == 0, DLMC_E_FORMAT, "bad chunk offsets");
@@ -764,11 +774,11 @@ static void read_payloads(const uint8_t* in, uint64_t len, const ContainerInfo& 
   const uint8_t* section = in + ci.hdr;
   if (ci.cp.coder == DLMC_CODER_RANK) {
     // context and varint ranks take at most 11 bytes a token
-    DLMC_CHECK(ci.total <= 16 * ci.n + 1024, DLMC_E_FORMAT, "bad payload size");
+    DLMC_CHECK(ci.total <= 1024 || (ci.total - 1024) / 16 <= ci.n, DLMC_E_FORMAT, "bad payload size");
     unpacked = decompress_block(ci.cp.rank_compressor, in + ci.hdr, len - ci.hdr, ci.total);
     section = unpacked.data();
   } else {
-    DLMC_CHECK(ci.hdr + ci.total <= len, DLMC_E_FORMAT, "bad chunk offsets");
+    DLMC_CHECK(ci.total <= len - ci.hdr, DLMC_E_FORMAT, "bad chunk offsets");
   }
   pls.assign(nc, {});
   crc.assign((ci.cp.flags & DLMC_FLAG_CRC) ? nc : 0, 0u);

@@ -127,10 +127,11 @@ def test_host_rans_rejects_bad_input():
 
 # ---------------------------------------------------------------- container header
 def make_container(payloads, n_tokens, chunk_len, first=0, count=None, numerics=None, crc=None,
-                   flags=0, seed=7, tau=float("-inf")):
+                   flags=0, seed=7, tau=float("-inf"), rank_compressor=None, level=6):
     """A version-3 container written field by field from the layout that
-    include/dlmc.h documents (range coder, so the payload section is stored
-    as is)."""
+    include/dlmc.h documents: the range coder, whose payload section is
+    stored as is, or (rank_compressor "none", "zlib", "lzma", "zstd") the
+    symbol ranking back end, whose section is compressed as one block."""
     import struct
     n_chunks = -(-n_tokens // chunk_len)
     count = len(payloads) if count is None else count
@@ -142,7 +143,12 @@ def make_container(payloads, n_tokens, chunk_len, first=0, count=None, numerics=
     struct.pack_into("<QQQQ", fixed, 16, 0x1234, seed, n_tokens, n_chunks)
     struct.pack_into("<iiiiifiiii", fixed, 48, chunk_len, 16, 32, 4, 4, tau, 1, 0, 0, 0)
     struct.pack_into("<d", fixed, 88, 1.0)
-    struct.pack_into("<iiiiiI", fixed, 96, 0, 0, 0, 0, 0, 0)
+    kinds = {"none": 0, "zlib": 1, "lzma": 2, "zstd": 3}
+    if rank_compressor is None:
+        struct.pack_into("<iiiiiI", fixed, 96, 0, 0, 0, 0, 0, 0)
+    else:
+        lv = 0 if rank_compressor == "none" else level
+        struct.pack_into("<iiiiiI", fixed, 96, 2, 0, 0, kinds[rank_compressor], lv, 0)
     struct.pack_into("<QQQ", fixed, 120, numerics, first, count)
     offs = [0]
     for p in payloads:
@@ -152,7 +158,11 @@ def make_container(payloads, n_tokens, chunk_len, first=0, count=None, numerics=
         tail += b"".join(struct.pack("<I", c) for c in crc)
     hdr = 144 + len(tail)
     struct.pack_into("<I", fixed, 8, hdr)
-    return bytes(fixed) + tail + b"".join(payloads)
+    section = b"".join(payloads)
+    if rank_compressor is not None:
+        from oracle import ranking as R
+        section = R.compress(section, rank_compressor, 0 if rank_compressor == "none" else level)
+    return bytes(fixed) + tail + section
 
 
 def test_numerics_id_is_recorded_and_checked():
@@ -215,3 +225,85 @@ def test_merge_rejects_parts_that_do_not_tile(case):
     with pytest.raises(dl.DlmcError) as e:
         dl.merge(parts)
     assert e.value.code == -4, case
+
+
+def test_header_sizes_cannot_wrap():
+    """Header fields chosen so that a size computed from them would wrap
+    around 2^64 are refused with E_FORMAT, without reading past the buffer:
+    2^61 - 1 one-token chunks (an offset table of 2^64 bytes, which wraps to a
+    144-byte header), a token count next to 2^64 (whose rounded-up chunk
+    count wraps to 0), and a payload section of 2^64 - 8 bytes."""
+    import struct
+    good = make_container([b"ab", b"c"], 8, 4)
+    n = (1 << 61) - 1
+    bad = bytearray(good[:144])
+    struct.pack_into("<QQ", bad, 32, n, n)     # n_tokens, n_chunks
+    struct.pack_into("<i", bad, 48, 1)         # chunk_len
+    struct.pack_into("<QQ", bad, 128, 0, n)    # first, count
+    struct.pack_into("<I", bad, 8, 144)        # header size
+    for blob in (bytes(bad), bytes(bad) + bytes(8)):
+        for call in (dl.decode_size, lambda b: dl.merge([b])):
+            with pytest.raises(dl.DlmcError) as e:
+                call(blob)
+            assert e.value.code == -4
+    bad = bytearray(make_container([], 0, 4))
+    struct.pack_into("<Q", bad, 32, (1 << 64) - 1)  # n_tokens; (n + 3) / 4 wraps to 0
+    with pytest.raises(dl.DlmcError) as e:
+        dl.decode_size(bytes(bad))
+    assert e.value.code == -4
+    bad = bytearray(make_container([b"x"], 4, 4))
+    struct.pack_into("<Q", bad, 152, (1 << 64) - 8)  # offsets[1]: the section's size
+    with pytest.raises(dl.DlmcError) as e:
+        dl.merge([bytes(bad)])
+    assert e.value.code == -4
+
+
+@pytest.mark.parametrize("kind", [None, "none", "zlib", "lzma", "zstd"])
+def test_container_damage_fails_cleanly(kind):
+    """Seeded random damage to valid containers -- bytes flipped, the end cut
+    or extended, header fields and chunk offsets set to random or extreme
+    values -- through decode_size and merge: each call returns or raises
+    DlmcError (format or corrupt, or invalid argument for an empty buffer);
+    none crashes or reads past the buffer."""
+    import struct
+    from oracle import ranking as R
+    if kind == "zstd" and R.zstd_library() is None:
+        pytest.skip("libzstd is not installed")
+    pls = [b"chunk-zero", b"c1", b"", b"third chunk payload", b"z"]
+    good = make_container(pls, 5 * 8 - 3, 8, crc=[1, 2, 3, 4, 5], rank_compressor=kind)
+    once = dl.merge([good])
+    # merge recompresses the section; liblzma's one-shot encoder writes the
+    # block sizes into its header, Python's streaming encoder does not
+    assert dl.merge([once]) == once and (kind == "lzma" or once == good)
+    rng = np.random.default_rng(11)
+    fields = [8, 32, 40, 48, 128, 136] + [144 + 8 * c for c in range(6)]
+    extremes = [0, 1, 2, 7, 8, 0x7FFFFFFF, 0x80000000, 0xFFFFFFFF, 1 << 32, 1 << 61, 1 << 63,
+                (1 << 64) - 8, (1 << 64) - 1]
+    outcomes = {"ok": 0, "error": 0}
+    for trial in range(1500):
+        blob = bytearray(good)
+        how = trial % 4
+        if how == 0:
+            for _ in range(int(rng.integers(1, 5))):
+                blob[int(rng.integers(0, len(blob)))] ^= int(rng.integers(1, 256))
+        elif how == 1:
+            blob = blob[: int(rng.integers(0, len(blob)))]
+        elif how == 2:
+            blob += bytes(rng.integers(0, 256, size=int(rng.integers(1, 64)), dtype=np.uint8))
+        else:
+            off = fields[int(rng.integers(0, len(fields)))]
+            v = extremes[int(rng.integers(0, len(extremes)))] if rng.integers(0, 2) else \
+                int(rng.integers(0, 1 << 63))
+            if off == 8 or off == 48:
+                struct.pack_into("<I", blob, off, v & 0xFFFFFFFF)
+            else:
+                struct.pack_into("<Q", blob, off, v)
+        for call in (dl.decode_size, lambda b: dl.merge([b])):
+            try:
+                call(bytes(blob))
+                outcomes["ok"] += 1
+            except dl.DlmcError as e:
+                # an empty buffer reaches the library as a NULL pointer (E_INVAL)
+                assert e.code in (-4, -5) or (e.code == -1 and not blob), (trial, e)
+                outcomes["error"] += 1
+    assert outcomes["error"] > 1000
