@@ -485,6 +485,38 @@ def test_device_decoder_corrupt_streams(coder, W):
             assert np.array_equal(m.decode(data), toks)
 
 
+def test_decode_damaged_containers():
+    """Seeded random damage anywhere in a container -- the header's codec
+    fields and chunk offsets included -- through the GPU decoder (range coder
+    and rANS, bf16 model, batch 2).  Every launch size comes from fields that
+    the header checks bound by the model (chunk length, batch, m_max, CDF
+    bits, context), so each decode returns some tokens or raises a format,
+    corrupt, buffer or argument error (codec fields out of range), never a
+    device error; the intact container still decodes."""
+    sh = shape()
+    toks = wl.markov1_tokens(90, sh.vocab, 12)
+    rng = np.random.default_rng(5)
+    with dl.Model(sh, max_chunk=32, max_batch=2) as m:
+        for coder in ("range", "rans"):
+            cd = codec(32, k=4, batch=2, coder=coder)
+            data = m.encode(toks, cd)
+            for trial in range(30):
+                bad = bytearray(data)
+                if trial % 3 == 2:
+                    bad = bad[: int(rng.integers(1, len(bad)))]
+                else:
+                    for _ in range(int(rng.integers(1, 4))):
+                        bad[int(rng.integers(0, len(bad)))] ^= int(rng.integers(1, 256))
+                log("damaged container", coder, trial)
+                try:
+                    m.decode(bytes(bad))
+                except dl.DlmcError as e:
+                    # never E_DEVICE: no launch may fail
+                    assert e.code in (-1, -4, -5, -6), (coder, trial, e)
+            log("intact", coder)
+            assert np.array_equal(m.decode(data), toks)
+
+
 def test_stage_profile_mask():
     """Only the stages named in the profile mask are timed; the CDF stage's
     work is filled in only when it is itself timed."""
