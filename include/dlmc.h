@@ -224,9 +224,14 @@ dlmc_status dlmc_decode_size(const uint8_t* in, uint64_t len, uint64_t* n_tokens
 dlmc_status dlmc_numerics_id(uint64_t* id);
 /* Decompress host container in[0..len) into host tokens[0..cap).  The codec
  * parameters come from the header; the batch used is `batch` when > 0, else
- * the header's.  E_FORMAT if the container was made by a model with another
- * configuration or seed; E_CORRUPT on an undecodable stream or CRC mismatch;
- * E_BUFFER if cap is too small (*n = required). */
+ * the header's.  The payload section is copied to device memory once and,
+ * with the range coder or rANS, every pass's symbols are decoded on the
+ * device (one wave per chunk of the batch, the host decoders' integer
+ * arithmetic), so CDF rows never leave the GPU.  E_FORMAT if the container
+ * was made by a model with another configuration or seed, or its header is
+ * inconsistent with its length; E_CORRUPT on an undecodable stream or CRC
+ * mismatch; E_BUFFER if cap is too small (*n = required, checked before any
+ * allocation). */
 dlmc_status dlmc_decode(dlmc_model* model, const uint8_t* in, uint64_t len, int32_t batch,
                         int32_t* tokens, uint64_t cap, uint64_t* n);
 
@@ -343,7 +348,7 @@ dlmc_status dlmc_weight_copy(dlmc_model* model, int32_t tensor_id, void* dst, ui
 #define DLMC_STAGE_ENTROPY 8
 #define DLMC_STAGE_SELECT 9
 #define DLMC_STAGE_CDF 10
-#define DLMC_STAGE_REVEAL 11
+#define DLMC_STAGE_REVEAL 11   /* encode: (start, freq) gather; decode: entropy decoder; reveal */
 #define DLMC_STAGE_COMPACT 12
 #define DLMC_N_STAGES 13
 #define DLMC_PROFILE_ALL ((1u << DLMC_N_STAGES) - 1u)
