@@ -215,7 +215,7 @@ struct dlmc_session {
   int32_t* h_pos = nullptr;
   int32_t* h_err = nullptr;
   uint32_t* h_sym = nullptr;
-  uint32_t* h_cdf = nullptr;  // trace: sel_cap * (V+1) per slot
+  uint32_t* h_cdf = nullptr;  // trace only (allocated on first use): m_max * (V+1)
   int32_t* h_dec = nullptr;
   int64_t* h_base = nullptr;
   int32_t* h_state = nullptr;   // max_batch * max_chunk: a slot's initial state

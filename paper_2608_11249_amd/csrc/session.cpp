@@ -454,6 +454,8 @@ int dlmc_session::step(uint64_t* coded) {
     const int ns = h_nsel[b];
     const uint32_t* rows_cdf = nullptr;
     if (!rank && m->trace) {
+      // the trace's CDF hash: the only use of the rows on the host
+      if (!h_cdf) pinned((void**)&h_cdf, (size_t)mm * row_words * 4);
       DLMC_HIP(hipMemcpy(h_cdf, m->cdf + (size_t)b * mm * row_words, (size_t)ns * row_words * 4,
                          hipMemcpyDeviceToHost));
       rows_cdf = h_cdf;
@@ -667,7 +669,6 @@ static void session_common(dlmc_session* s, dlmc_model* m, const dlmc_codec_para
   pinned((void**)&s->h_sym, slots * 8);
   pinned((void**)&s->h_dec, slots * 4);
   pinned((void**)&s->h_base, (size_t)m->cfg.max_batch * 8);
-  pinned((void**)&s->h_cdf, (size_t)cp.m_max * ((size_t)m->cfg.vocab + 1) * 4);
   pinned((void**)&s->h_state, (size_t)m->cfg.max_batch * m->cfg.max_chunk * 4);
   pinned((void**)&s->h_rows, slots * 4);
   pinned((void**)&s->h_selpos, slots * 4);
