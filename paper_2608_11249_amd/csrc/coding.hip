@@ -1,6 +1,7 @@
 // Coding stages of one masked-diffusion step: masked-row compaction,
 // per-position entropy, the entropy-based commitment schedule, integer CDF
-// quantisation and the reveal of committed symbols.
+// quantisation, the decoders' symbol search (decode) and the reveal of
+// committed symbols.
 //
 // All reductions use fixed trees (wave butterflies, then wave totals in order)
 // and the CDF is integer arithmetic after one expf per entry, so encode and

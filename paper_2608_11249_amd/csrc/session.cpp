@@ -8,7 +8,9 @@
 // Chunks are independent windows; up to `batch` of them share a forward pass,
 // and a slot whose chunk is done takes the next one.  Every kernel computes a
 // chunk's values independently of the other chunks in the batch, so the
-// batch size does not change the output.
+// batch size does not change the output.  Encoding codes on the host from
+// each committed symbol's (start, freq); decoding runs the range or rANS
+// decoder on the device (decode_symbols), so CDF rows stay in HBM.
 #include <cmath>
 #include <cstring>
 
