@@ -3,9 +3,12 @@ progressive), the rANS coder and the initial context, through the C ABI.
 
 Block schedules fix their positions in advance, so the GPU and the oracle
 follow the same trajectory: selections and stored contexts are compared
-exactly, code lengths within 0.5%.
+exactly, and the information content of the coded symbols (sum -log2 q, q
+= f / 2^P) within 0.5% of the oracle's along the GPU's trajectory, with no
+additive slack.
 """
 import dataclasses
+import math
 
 import numpy as np
 import pytest
@@ -35,32 +38,41 @@ TINY_CASES = [
 @pytest.mark.parametrize("kw", TINY_CASES)
 def test_tiny_against_oracle(kw):
     """fp32 tiny model, two 256-byte chunks: same selections and contexts as
-    the oracle, code length within 0.5%, exact round trip."""
+    the oracle; along the GPU's trajectory the coded symbols' information
+    content sum -log2 (f / 2^P) is within 0.5% of the oracle's (no additive
+    slack); exact round trip."""
     w = wl.WORKLOADS["tiny"]
     cd = dataclasses.replace(w.codec, batch=2, **kw)
     toks = wl.make_tokens(w, 512)
     log("tiny vs oracle", kw)
-    sel = {}
+    sel, coded = {}, {}
 
-    def tr(d, chunk, pas, pos, ent, h):
+    def tr(d, chunk, pas, pos, ent, iv, h):
         if d == 0:
             sel[(chunk, pas)] = tuple(pos)
+            coded[(chunk, pas)] = tuple(iv)
 
     with dl.Model(w.model, max_chunk=256, max_batch=2) as m:
-        m.set_trace(tr)
+        m.set_trace(tr, coded=True)
         data = m.encode(toks, cd)
         m.set_trace(None)
         assert np.array_equal(m.decode(data, batch=1), toks)
     W = OW.Weights(w.model)
     res = OD.encode(w.model, W, toks, cd)
+    P = cd.cdf_bits
     for c, (r, gp) in enumerate(zip(res, payloads(data))):
         ctx = min(cd.context, 256)
         assert gp[: 6 * ctx] == r.payload[: 6 * ctx]            # stored context, bit-exact
+        n_pass = sum(1 for (cc, _) in sel if cc == c)
         if cd.schedule != "entropy":
             assert [sel[(c, p)] for p in range(r.passes)] == [tuple(s.tolist()) for s in r.selections]
-            assert (c, r.passes) not in sel
-        g, o = len(gp) - 6 * ctx, len(r.payload) - 6 * ctx
-        assert abs(g - o) <= 0.005 * o + 12, (g, o)
+            assert n_pass == r.passes
+        forced = [np.array(sel[(c, p)], dtype=np.int64) for p in range(n_pass)]
+        along = OD.encode_chunk(w.model, W, toks[c * 256:(c + 1) * 256], cd, forced=forced, chunk_index=c)
+        gpu_bits = sum(P - math.log2(f) for p in range(n_pass) for _, f in coded[(c, p)])
+        rel = abs(gpu_bits - along.ideal_bits) / along.ideal_bits
+        log(f"chunk {c}: {gpu_bits:.3f} vs oracle {along.ideal_bits:.3f} bits, rel {rel:.2e}")
+        assert rel <= 0.005
 
 
 @pytest.mark.parametrize("kw", [
