@@ -1009,11 +1009,21 @@ void gemm_bf16(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, i
   static const double c0_w256[5] = {21.5, 50.7, 18.3, 25.9, 7.0};
   static const double c0_192[5] = {17.9, 20.5, 9.0, 9.7, 5.0};
   const double nk = (double)K / BK;
-  auto t_of = [&](int bm, int bn, long slots, double c0, double c1, long cols) -> double {
+  // c0s: the fixed cost of a wave of tiles that follows another, where it
+  // differs from the first wave's
+  auto t_of = [&](int bm, int bn, long slots, double c0, double c1, long cols, double c0s = -1.0) -> double {
     if (cols <= 0) return 0.0;
     const long tiles = (long)ceil_div(live, bm) * ceil_div((int)cols, bn);
-    return (double)((tiles + slots - 1) / slots) * (c0 + nk * c1);
+    const double waves = (double)((tiles + slots - 1) / slots);
+    return waves * nk * c1 + c0 + (waves - 1.0) * (c0s >= 0.0 ? c0s : c0);
   };
+  // The residual update of 256 x 128 tiles: in a launch of one wave every
+  // tile's fp32 read and write of the residual rows happen at once (c0); in
+  // later waves they overlap other tiles' main loops, the more so the longer
+  // the main loop (about 12.9, 5.8 and 3.3 us per wave at K = 768, 4096 and
+  // 12288, M = 65536).
+  const double c0s_w128 =
+      epi == EPI_RESIDUAL ? c0_w128[ei] * std::min(1.0, std::sqrt(768.0 / (double)K)) : -1.0;
   const double t128 = t_of(128, 128, 512, c0_128[ei], 1.26, N);
   // 192 x 128: QKV tiles must lie inside Q, K or V (d % 128 == 0 holds)
   const double t192 = t_of(192, 128, 512, c0_192[ei], 1.253, N);
@@ -1023,7 +1033,7 @@ void gemm_bf16(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, i
   const bool wide_ok = epi != EPI_QKV_ROPE || ea.d % 256 == 0;
   if (N % 128 == 0) {
     auto t_split = [&](int c1) {
-      return t_of(256, 256, 256, c0_w256[ei], 1.53, c1) + t_of(256, 128, 256, c0_w128[ei], 0.98, N - c1);
+      return t_of(256, 256, 256, c0_w256[ei], 1.53, c1) + t_of(256, 128, 256, c0_w128[ei], 0.98, N - c1, c0s_w128);
     };
     // one tile shape (all 256 x 128, or all 256 x 256), then a split if it
     // is more than 3% faster (the estimate rounds each part up to whole
