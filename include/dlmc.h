@@ -276,6 +276,18 @@ dlmc_status dlmc_test_inject_nonfinite(dlmc_model* model, int32_t on);
  * another mode. */
 dlmc_status dlmc_test_head_logits(dlmc_model* model, int32_t mode);
 
+/* Test hook (host only, no GPU needed): the tile shape the bf16 GEMM chooses
+ * for an M x N x K product with epilogue `epi` (0 fp32 store, 1 residual
+ * update, 2 QKV with rotary, 3 GELU, 4 SwiGLU; d_model is the QKV
+ * epilogue's model width, else unused).  *kind: 0 128 x 128 tiles, 1
+ * 192 x 128 tiles (two blocks per CU), 2 the 4-wave kernel with columns
+ * [0, *split) on 256 x 256 tiles and [*split, N) on 256 x 128 tiles.  The
+ * choice never changes a result; the GEMMs run in the forward pass of
+ * Definition 3.  E_INVAL for sizes the GEMM does not take (K % 64 != 0,
+ * M, N < 1, paired epilogues with N % 128 != 0) or a NULL output. */
+dlmc_status dlmc_test_gemm_tiles(int32_t M, int32_t N, int32_t K, int32_t epi, int32_t d_model,
+                                 int32_t* kind, int32_t* split);
+
 /* One forward pass (Definition 3) over device state[B*T] (int32, MASK =
  * vocab).  Writes the fp32 logits at the masked positions, in ascending
  * (chunk, position) order, to logits[n_rows * vocab], their flat indices

@@ -111,6 +111,8 @@ _SIGS = {
     "dlmc_numerics_id": (i32, [P(u64)]),
     "dlmc_test_inject_nonfinite": (i32, [vp, i32]),
     "dlmc_test_head_logits": (i32, [vp, i32]),
+    "dlmc_test_gemm_tiles": (i32, [i32, i32, i32, i32, i32, ctypes.POINTER(ctypes.c_int32),
+                                   ctypes.POINTER(ctypes.c_int32)]),
     "dlmc_status_string": (ctypes.c_char_p, [i32]),
     "dlmc_last_error": (ctypes.c_char_p, []),
 }
@@ -437,6 +439,18 @@ class Model:
         out = np.empty((rows, cols), dtype=dt)
         _check(lib().dlmc_weight_copy(self.handle, tensor_id, _ptr(out), out.nbytes))
         return out
+
+
+GEMM_EPI = {"store": 0, "residual": 1, "qkv": 2, "gelu": 3, "swiglu": 4}
+
+
+def gemm_tiles(M: int, N: int, K: int, epi: str, d_model: int = 0):
+    """(kind, split) the bf16 GEMM chooses (host only): kind "128x128",
+    "192x128" or "4wave" with columns [0, split) on 256 x 256 tiles."""
+    kind, split = ctypes.c_int32(), ctypes.c_int32()
+    _check(lib().dlmc_test_gemm_tiles(M, N, K, GEMM_EPI[epi], d_model, ctypes.byref(kind),
+                                      ctypes.byref(split)))
+    return ("128x128", "192x128", "4wave")[kind.value], split.value
 
 
 def decode_size(data: bytes) -> int:

@@ -244,6 +244,20 @@ dlmc_status dlmc_test_head_logits(dlmc_model* m, int32_t mode) {
   });
 }
 
+dlmc_status dlmc_test_gemm_tiles(int32_t M, int32_t N, int32_t K, int32_t epi, int32_t d_model,
+                                 int32_t* kind, int32_t* split) {
+  return guard([&] {
+    DLMC_CHECK(kind && split, DLMC_E_INVAL, "NULL argument");
+    DLMC_CHECK(M >= 1 && N >= 1 && K >= 64 && K % 64 == 0 && epi >= 0 && epi <= 4, DLMC_E_INVAL,
+               "sizes or epilogue the bf16 GEMM does not take");
+    DLMC_CHECK((epi != EPI_QKV_ROPE && epi != EPI_SWIGLU) || N % 128 == 0, DLMC_E_INVAL,
+               "paired epilogue needs N % 128 == 0");
+    const GemmTiles t = gemm_bf16_tiles(M, N, K, (EpiKind)epi, d_model, -1);
+    *kind = t.kind;
+    *split = t.split;
+  });
+}
+
 dlmc_status dlmc_forward_logits(dlmc_model* m, const int32_t* state, int32_t B, int32_t T,
                                 float* logits, int32_t* rows, int32_t* n_rows) {
   return guard([&] {

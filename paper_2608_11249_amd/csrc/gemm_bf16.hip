@@ -976,17 +976,7 @@ void launch(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int 
 
 }  // namespace
 
-void gemm_bf16(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int K,
-               const int* M_dev, EpiKind epi, const EpiArgs& ea, int rows_hint) {
-  DLMC_CHECK(K % BK == 0 && K > 0, DLMC_E_INVAL, "bf16 GEMM needs K % 64 == 0");
-  DLMC_CHECK((int64_t)M * K < (1ll << 31) && (int64_t)N * K < (1ll << 31), DLMC_E_INVAL,
-             "GEMM operand too large for 32-bit offsets");
-  if (M <= 0 || N <= 0) return;
-  DLMC_CHECK(!ea.stats || epi == EPI_STORE_F32, DLMC_E_INVAL, "row statistics need the fp32 store");
-  const bool paired = (epi == EPI_QKV_ROPE || epi == EPI_SWIGLU);
-  DLMC_CHECK(!paired || N % 128 == 0, DLMC_E_INVAL, "paired epilogue needs N % 128 == 0");
-  DLMC_CHECK(epi != EPI_QKV_ROPE || (ea.d % 128 == 0 && (ea.dh == 64 || ea.dh == 128)),
-             DLMC_E_INVAL, "QKV epilogue needs d % 128 == 0 and head dim 64 or 128");
+GemmTiles gemm_bf16_tiles(int M, int N, int K, EpiKind epi, int d, int rows_hint) {
   // Tile choice (never changes the result).  Estimated time of an option:
   // waves of tiles x (c0 + k-tiles x c1), where c1 is a tile's main-loop time
   // per 64-wide k-tile with every CU busy, and c0 its fixed cost (prologue
@@ -1030,7 +1020,7 @@ void gemm_bf16(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, i
   double t4 = 1e300;
   int split = -1;  // columns on 256 x 256 tiles
   // a QKV tile must lie inside one of Q, K, V: 256-wide tiles need d % 256 == 0
-  const bool wide_ok = epi != EPI_QKV_ROPE || ea.d % 256 == 0;
+  const bool wide_ok = epi != EPI_QKV_ROPE || d % 256 == 0;
   if (N % 128 == 0) {
     auto t_split = [&](int c1) {
       return t_of(256, 256, 256, c0_w256[ei], 1.53, c1) + t_of(256, 128, 256, c0_w128[ei], 0.98, N - c1, c0s_w128);
@@ -1052,14 +1042,31 @@ void gemm_bf16(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, i
       }
     }
   }
-  if (t192 < t128 && (split < 0 || t192 < t4)) {
+  if (t192 < t128 && (split < 0 || t192 < t4)) return {GEMM_TILES_192x128, 0};
+  if (split >= 0 && t4 <= t128) return {GEMM_TILES_4WAVE, split};
+  return {GEMM_TILES_128x128, 0};
+}
+
+void gemm_bf16(hipStream_t st, const bf16_t* A, const bf16_t* B, int M, int N, int K,
+               const int* M_dev, EpiKind epi, const EpiArgs& ea, int rows_hint) {
+  DLMC_CHECK(K % BK == 0 && K > 0, DLMC_E_INVAL, "bf16 GEMM needs K % 64 == 0");
+  DLMC_CHECK((int64_t)M * K < (1ll << 31) && (int64_t)N * K < (1ll << 31), DLMC_E_INVAL,
+             "GEMM operand too large for 32-bit offsets");
+  if (M <= 0 || N <= 0) return;
+  DLMC_CHECK(!ea.stats || epi == EPI_STORE_F32, DLMC_E_INVAL, "row statistics need the fp32 store");
+  const bool paired = (epi == EPI_QKV_ROPE || epi == EPI_SWIGLU);
+  DLMC_CHECK(!paired || N % 128 == 0, DLMC_E_INVAL, "paired epilogue needs N % 128 == 0");
+  DLMC_CHECK(epi != EPI_QKV_ROPE || (ea.d % 128 == 0 && (ea.dh == 64 || ea.dh == 128)),
+             DLMC_E_INVAL, "QKV epilogue needs d % 128 == 0 and head dim 64 or 128");
+  const GemmTiles tc = gemm_bf16_tiles(M, N, K, epi, ea.d, rows_hint);
+  if (tc.kind == GEMM_TILES_192x128) {
     launch<192, 128>(st, A, B, M, N, K, M_dev, epi, ea);
-  } else if (split >= 0 && t4 <= t128) {
-    if (split > 0 && split < N) {
-      launch_split(st, A, B, M, N, K, M_dev, epi, ea, split);
+  } else if (tc.kind == GEMM_TILES_4WAVE) {
+    if (tc.split > 0 && tc.split < N) {
+      launch_split(st, A, B, M, N, K, M_dev, epi, ea, tc.split);
     } else {
-      launch_256<256>(st, A, B, M, N, K, M_dev, epi, ea, 0, split);
-      launch_256<128>(st, A, B, M, N, K, M_dev, epi, ea, split, N);
+      launch_256<256>(st, A, B, M, N, K, M_dev, epi, ea, 0, tc.split);
+      launch_256<128>(st, A, B, M, N, K, M_dev, epi, ea, tc.split, N);
     }
   } else {
     launch<128, 128>(st, A, B, M, N, K, M_dev, epi, ea);

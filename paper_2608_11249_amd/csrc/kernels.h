@@ -31,6 +31,16 @@ struct EpiArgs {
   int stat_ld = 0;
 };
 
+// Tile shape of a bf16 GEMM (the choice never changes the result):
+// 128 x 128 or 192 x 128 tiles two blocks per CU, or the 4-wave kernel with
+// columns [0, split) on 256 x 256 tiles and [split, N) on 256 x 128 tiles.
+enum GemmTileKind { GEMM_TILES_128x128 = 0, GEMM_TILES_192x128 = 1, GEMM_TILES_4WAVE = 2 };
+struct GemmTiles {
+  int kind, split;
+};
+// the choice gemm_bf16 makes for these sizes (d: the QKV epilogue's model
+// width); host only
+GemmTiles gemm_bf16_tiles(int M, int N, int K, EpiKind epi, int d, int rows_hint);
 // M_dev (optional): device int holding the live row count (<= M); rows at or
 // beyond it are neither computed (whole tiles) nor stored.  rows_hint: the
 // live row count if the host knows it (tile selection only), else -1.
